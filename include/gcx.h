@@ -1,0 +1,193 @@
+/*
+ * gcx.h -- C ABI of the partial-straggler gradient-coding hot path on MI355X (gfx950).
+ *
+ * Implements, for one GPU holding all m simulated workers, the data-parallel
+ * steps of the gradient-coding protocol of "Leveraging partial stragglers
+ * within gradient coding" (Ramamoorthy, Meng, Girimaji):
+ *
+ *   gc_assign         assignment support and chunk order        (Sec. 1; Sec. 3)
+ *   gc_chunk_grads    per-chunk gradients g_{D_i}               (Sec. 1)
+ *   gc_sum_chunks     the exact target  sum_i g_{D_i}           (Sec. 1)
+ *   gc_decode_coeffs  coverage, decodability and Algorithm 1    (Sec. 2; Sec. 2.1)
+ *   gc_encode         each worker's transmitted vector g_beta   (Sec. 2)
+ *   gc_reconstruct    the PS combine  sum_j R[k][j] g_j         (Sec. 2.2)
+ *
+ * Conventions (every entry point):
+ *   - Row-major arrays, 0-based indices.  Chunk i is the paper's D_{i+1},
+ *     worker j is W_{j+1}; positions inside a worker are 0-based (the paper's
+ *     ordering matrix O keeps 1-based positions, 0 = not assigned).
+ *   - The caller owns every buffer.  Pointers documented "device" must be
+ *     device memory of the current HIP device; "host" pointers are host memory.
+ *     Nothing is allocated by the library except what a workspace argument
+ *     brings in; no handle or global state is kept between calls.
+ *   - Device entry points enqueue work on `stream` (0 = the null stream) and
+ *     return without synchronising; outputs are valid once the caller has
+ *     synchronised the stream.  Calls on one stream are ordered.
+ *   - Return value: GC_OK, or a negative status.  Arguments are validated on
+ *     the host before anything is launched; a non-OK return from validation
+ *     means nothing was enqueued.  Nothing is printed.
+ *   - The communication factor ell satisfies 1 <= ell <= GC_MAX_ELL.  A
+ *     gradient of length d is cut into ell contiguous blocks of length
+ *     L = ceil(d / ell); block k covers entries [k*L, (k+1)*L) of the gradient
+ *     zero-padded to length ell*L.
+ */
+#ifndef GCX_H
+#define GCX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define GC_OK 0
+#define GC_EINVAL (-1)  /* bad size, null pointer, bad enum, inconsistent tables  */
+#define GC_ELAUNCH (-2) /* the HIP runtime reported an error at launch           */
+#define GC_ENOTSUP (-3) /* the current device is not gfx950                      */
+
+/* assignment kinds for gc_assign */
+#define GC_ASSIGN_CYCLIC 0 /* cyclic scheme, N = m, worker j holds j..j+s (mod N) */
+#define GC_ASSIGN_ORDER 1  /* tables derived from a caller-given ordering matrix O */
+
+/* losses for gc_chunk_grads */
+#define GC_LOSS_LINEAR 0   /* l = (x.w - y)^2 / 2           */
+#define GC_LOSS_LOGISTIC 1 /* l = log(1 + e^{x.w}) - y x.w  */
+
+/* storage types of chunk gradients */
+#define GC_F32 0
+#define GC_BF16 1 /* bfloat16, accumulated in fp32 */
+
+/* values of dec[] written by gc_decode_coeffs */
+#define GC_DEC_NO 0      /* some chunk has fewer than ell processed copies    */
+#define GC_DEC_YES 1     /* every chunk has at least ell processed copies      */
+#define GC_DEC_INVALID 2 /* psi had an entry outside [0, delta_j]; Bc zeroed   */
+
+#define GC_MAX_ELL 8
+#define GC_MAX_M 1024     /* workers            */
+#define GC_MAX_DELTA 64   /* table widths       */
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int gc_version(void);
+
+/* Short static description of a status code. */
+const char *gc_strerror(int status);
+
+/*
+ * gc_assign -- host only.  The assignment matrix A (Sec. 1, "Background") is
+ * described by its support and the order in which each worker processes its
+ * chunks, the ordering matrix O of Sec. 3: O[i*m + j] = 0 if chunk i is not
+ * assigned to worker j, else its 1-based position inside worker j.
+ *
+ * kind = GC_ASSIGN_CYCLIC: requires N == m and 0 <= s < m; worker j holds
+ *   chunks j, j+1, ..., j+s (mod N) in that order (the cyclic scheme whose
+ *   ordering Sec. 3 states is optimal for exact GC).  Writes O (if non-NULL).
+ *   delta and gamma must both equal s + 1.
+ * kind = GC_ASSIGN_ORDER: O is an input; every column's non-zero entries must
+ *   be 1..delta_j, once each (Sec. 3).  s is ignored.  delta >= max_j delta_j
+ *   and gamma >= max_i gamma_i.
+ *
+ * Outputs (host, int32, -1 padded past a row's length):
+ *   order  [m][delta]  chunk at position t of worker j
+ *   holder [N][gamma]  u-th worker holding chunk i, ascending worker index
+ *   hpos   [N][gamma]  position of chunk i inside worker holder[i][u]
+ * Errors: GC_EINVAL for a null table pointer, bad sizes, an O that is not an
+ * ordering matrix, or tables too narrow.
+ */
+int gc_assign(int32_t kind, int32_t N, int32_t m, int32_t s, int32_t *O, int32_t delta,
+              int32_t gamma, int32_t *order, int32_t *holder, int32_t *hpos);
+
+/*
+ * gc_chunk_grads -- per-chunk gradients (Sec. 1: g_{D_i} is the sum over the
+ * samples of chunk i of the per-sample gradient) at b evaluation points:
+ *   G[q][i][:] = X_i^T r,  r = X_i w_q - y_i          (GC_LOSS_LINEAR)
+ *                          r = sigmoid(X_i w_q) - y_i (GC_LOSS_LOGISTIC)
+ * X [N][n][d], y [N][n], W [b][d], G [b][N][d]: device fp32.  fp32 arithmetic.
+ * workspace: device, at least gc_chunk_grads_workspace_size(N, n, d, b) bytes
+ * (may be NULL when that size is 0).
+ * Errors: GC_EINVAL for sizes < 1, a null pointer, an unknown loss, or a
+ * workspace that is too small.
+ */
+size_t gc_chunk_grads_workspace_size(int32_t N, int32_t n, int64_t d, int32_t b);
+int gc_chunk_grads(const float *X, const float *y, const float *W, int32_t N, int32_t n,
+                   int64_t d, int32_t b, int32_t loss, float *G, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * gc_sum_chunks -- gsum[x] = sum_i G[i][x], the gradient the PS wants
+ * (Sec. 1, grad L = sum_j g_{D_j}).  G [N][d] device in g_dtype; gsum [d]
+ * device fp32, accumulated in fp64 and rounded once.
+ */
+int gc_sum_chunks(const void *G, int32_t g_dtype, int32_t N, int64_t d, float *gsum,
+                  hipStream_t stream);
+
+/*
+ * gc_decode_coeffs -- for each straggler pattern p (a state vector psi of
+ * Sec. 2: worker j has processed the chunks at positions 0..psi[p][j]-1 of
+ * its order) compute, independently and in parallel:
+ *   cov[p][i]   Delta_i = number of workers that processed chunk i
+ *   dec[p]      GC_DEC_YES iff every Delta_i >= ell (the exact-GC condition of
+ *               Sec. 2 / Sec. 2.1), GC_DEC_NO otherwise, GC_DEC_INVALID if a
+ *               psi[p][j] lies outside [0, delta_j]
+ *   coef_err[p] sum_i max(0, ell - Delta_i) (the coefficient-space error of
+ *               Sec. 2.1)
+ *   Bc[p][j][t][k]  the encoding coefficient B^{(i)}_{j,k} of Algorithm 1 for
+ *               chunk i = order[j][t]: with S_i the processed holders of chunk
+ *               i and X = R[:, S_i] (ell x Delta_i), the rows of B^{(i)} on
+ *               S_i are the minimum-norm least-squares solution pinv(X); zero
+ *               for t >= psi[p][j], for padded table slots, and for the whole
+ *               pattern when dec[p] = GC_DEC_INVALID.
+ * The small solves run in fp64 (Gram matrix and Cholesky factorisation of
+ * size min(ell, Delta_i)); Bc is rounded to fp32 once.
+ * psi [P][m] int32, order [m][delta], holder/hpos [N][gamma] int32 (as from
+ * gc_assign, -1 padded), R [ell][m] fp32, cov [P][N] int32, dec [P] uint8,
+ * coef_err [P] int32, Bc [P][m][delta][ell] fp32: all device.
+ * Requires 1 <= m <= GC_MAX_M, 1 <= delta, gamma <= GC_MAX_DELTA.
+ * P = 0 is a no-op.  Invalid psi values are reported in dec, not by the return
+ * value (psi is device data and is not read on the host).
+ */
+int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m, const int32_t *order,
+                     int32_t delta, const int32_t *holder, const int32_t *hpos, int32_t gamma,
+                     const float *R, int32_t ell, int32_t *cov, uint8_t *dec, int32_t *coef_err,
+                     float *Bc, hipStream_t stream);
+
+/*
+ * gc_encode -- what every worker transmits (Sec. 2, worker encode): for each
+ * pattern p and worker j,
+ *   T[p][j][x] = sum_{t < psi[p][j]} sum_{k < ell} Bc[p][j][t][k] * g_{order[j][t]}[k*L + x]
+ * for 0 <= x < L, over the worker's processed prefix only (a worker with
+ * psi = 0 sends zeros).  G [N][d] device in g_dtype; psi [P][m], order
+ * [m][delta] int32 device; Bc [P][m][delta][ell] fp32 device (as from
+ * gc_decode_coeffs); T [P][m][L] fp32 device.  fp32 accumulation.  psi is
+ * clamped to [0, delta] and padded order slots are skipped.
+ */
+int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_t *psi,
+              const int32_t *order, const float *Bc, int64_t P, int32_t m, int32_t delta,
+              int32_t ell, float *T, hipStream_t stream);
+
+/*
+ * gc_reconstruct -- the PS combine (Sec. 2.2, last step): block k of the
+ * estimate is sum_j R[k][j] T[p][j][:], i.e.
+ *   ghat[p][k*L + x] = sum_j R[k][j] * T[p][j][x]   for k*L + x < d.
+ * Equals sum_i g_{D_i} when the pattern is decodable; otherwise it is the
+ * least-squares estimate.  If gsum is non-NULL and sqerr non-NULL,
+ *   sqerr[p] = sum_x (ghat[p][x] - gsum[x])^2   (fp64 accumulation)
+ * ghat may be NULL (error-only mode).  T [P][m][L], R [ell][m], ghat [P][d],
+ * gsum [d] fp32, sqerr [P] fp64: device.  workspace: device, at least
+ * gc_reconstruct_workspace_size(P, m, d, ell) bytes when sqerr is requested
+ * (it holds per-slice partial sums, reduced in a fixed order, so sqerr is
+ * deterministic).
+ */
+size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell);
+int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t m, int64_t d, int32_t ell,
+                   float *ghat, const float *gsum, double *sqerr, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GCX_H */

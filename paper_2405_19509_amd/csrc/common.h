@@ -1,0 +1,60 @@
+// Internal helpers shared by the gcx HIP sources (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "gcx.h"
+
+namespace gcx {
+
+constexpr int kWave = 64;
+
+// The library is built for gfx950 only; refuse other devices up front rather
+// than failing at the first launch with an opaque "invalid device function".
+inline int check_device() {
+  static int cached[64];  // 0 unknown, 1 ok, 2 not supported
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return GC_ELAUNCH;
+  if (dev >= 0 && dev < 64 && cached[dev]) return cached[dev] == 1 ? GC_OK : GC_ENOTSUP;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return GC_ELAUNCH;
+  const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  if (dev >= 0 && dev < 64) cached[dev] = ok ? 1 : 2;
+  return ok ? GC_OK : GC_ENOTSUP;
+}
+
+inline int launch_status() {
+  return hipGetLastError() == hipSuccess ? GC_OK : GC_ELAUNCH;
+}
+
+inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// bf16 bits -> fp32 (exact)
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+}  // namespace gcx

@@ -1,0 +1,284 @@
+// gc_decode_coeffs: coverage, decodability, coefficient error and the
+// encoding coefficients of Algorithm 1 (Find-Encoding-Coeff), batched over
+// straggler patterns.  One wavefront per pattern, one lane per chunk.
+//
+// For chunk i with processed holders S_i (Delta = |S_i|) and X = R[:, S_i]
+// (ell x Delta), Algorithm 1's minimum-norm least-squares coefficients are
+// the rows of pinv(X) (the Frobenius objective separates per column, Sec. 2.1
+// and the W_5 example of Sec. 2.2).  Each lane forms them in fp64 from the
+// smaller Gram matrix:
+//   Delta >= ell:  M = X X^T (ell x ell),  row j of pinv(X) = (M^-1 x_j)^T
+//   Delta <  ell:  H = X^T X (Delta x Delta, padded with the identity to
+//                  ell x ell),  pinv(X) = H^-1 X^T
+// with a Cholesky factorisation of M or H.  ell = 1 reduces to Remark 1:
+// coefficient R_j / sum_{S_i} R^2.  Coverage and decodability are integer
+// decisions and never depend on the floating-point solve.
+#include "common.h"
+
+namespace gcx {
+namespace {
+
+constexpr int kDecodeThreads = 256;
+constexpr int kDecodeWaves = kDecodeThreads / kWave;
+
+// In-place Cholesky factorisation of a symmetric positive-definite ELL x ELL
+// matrix (lower triangle used), fully unrolled so every index is static.
+template <int ELL>
+__device__ __forceinline__ void cholesky(double (&A)[ELL][ELL]) {
+#pragma unroll
+  for (int c = 0; c < ELL; ++c) {
+    double s = A[c][c];
+#pragma unroll
+    for (int q = 0; q < c; ++q) s -= A[c][q] * A[c][q];
+    const double dcc = sqrt(s);
+    A[c][c] = dcc;
+    const double inv = 1.0 / dcc;
+#pragma unroll
+    for (int r = c + 1; r < ELL; ++r) {
+      double v = A[r][c];
+#pragma unroll
+      for (int q = 0; q < c; ++q) v -= A[r][q] * A[c][q];
+      A[r][c] = v * inv;
+    }
+  }
+}
+
+// Solve (L L^T) z = b in place, L the lower factor from cholesky().
+template <int ELL>
+__device__ __forceinline__ void chol_solve(const double (&Lf)[ELL][ELL], double (&b)[ELL]) {
+#pragma unroll
+  for (int r = 0; r < ELL; ++r) {
+    double v = b[r];
+#pragma unroll
+    for (int q = 0; q < r; ++q) v -= Lf[r][q] * b[q];
+    b[r] = v / Lf[r][r];
+  }
+#pragma unroll
+  for (int r = ELL - 1; r >= 0; --r) {
+    double v = b[r];
+#pragma unroll
+    for (int q = r + 1; q < ELL; ++q) v -= Lf[q][r] * b[q];
+    b[r] = v / Lf[r][r];
+  }
+}
+
+template <int ELL>
+__global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
+    const int32_t *__restrict__ psi, int64_t P, int N, int m, const int32_t *__restrict__ order,
+    int delta, const int32_t *__restrict__ holder, const int32_t *__restrict__ hpos, int gamma,
+    const float *__restrict__ R, int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
+    int32_t *__restrict__ coef_err, float *__restrict__ Bc) {
+  extern __shared__ float Rs[];  // [ELL][m]
+  for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
+  __syncthreads();  // the only barrier; every thread reaches it
+
+  const int lane = threadIdx.x % kWave;
+  const int64_t p = int64_t(blockIdx.x) * kDecodeWaves + threadIdx.x / kWave;
+  if (p >= P) return;
+
+  const int32_t *ps = psi + p * m;
+  const int64_t wstride = int64_t(delta) * ELL;       // floats per worker in Bc
+  float *Bp = Bc + p * int64_t(m) * wstride;
+
+  // psi_j must lie in [0, delta_j]; padded order slots get zero coefficients.
+  bool bad = false;
+  for (int j = lane; j < m; j += kWave) {
+    int load = 0;
+    for (int t = 0; t < delta; ++t) {
+      const int c = order[int64_t(j) * delta + t];
+      if (c >= 0 && c < N) {
+        ++load;
+      } else {
+#pragma unroll
+        for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
+      }
+    }
+    const int v = ps[j];
+    bad = bad || v < 0 || v > load;
+  }
+  const bool invalid = __any(bad);
+
+  int err = 0;
+  bool all_ok = true;
+  for (int i = lane; i < N; i += kWave) {
+    const int32_t *hi = holder + int64_t(i) * gamma;
+    const int32_t *hp = hpos + int64_t(i) * gamma;
+    // W_j processed chunk i iff chunk i sits at a position t < psi_j of W_j
+    int Delta = 0;
+    for (int u = 0; u < gamma; ++u) {
+      const int j = hi[u], t = hp[u];
+      if (j >= 0 && j < m && t >= 0 && t < delta && ps[j] > t) ++Delta;
+    }
+    cov[p * N + i] = Delta;
+    err += Delta < ELL ? ELL - Delta : 0;
+    all_ok = all_ok && Delta >= ELL;
+
+    if (Delta == 0 || invalid) {
+      for (int u = 0; u < gamma; ++u) {
+        const int j = hi[u], t = hp[u];
+        if (j >= 0 && j < m && t >= 0 && t < delta) {
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
+        }
+      }
+      continue;
+    }
+
+    if constexpr (ELL == 1) {
+      double ss = 0.0;
+      for (int u = 0; u < gamma; ++u) {
+        const int j = hi[u], t = hp[u];
+        if (j >= 0 && j < m && t >= 0 && t < delta && ps[j] > t) {
+          const double x = Rs[j];
+          ss += x * x;
+        }
+      }
+      for (int u = 0; u < gamma; ++u) {
+        const int j = hi[u], t = hp[u];
+        if (j >= 0 && j < m && t >= 0 && t < delta)
+          Bp[j * wstride + t] = ps[j] > t ? float(double(Rs[j]) / ss) : 0.f;
+      }
+    } else if (Delta >= ELL) {
+      // M = X X^T, lower triangle
+      double M[ELL][ELL];
+#pragma unroll
+      for (int a = 0; a < ELL; ++a)
+#pragma unroll
+        for (int b = 0; b < ELL; ++b) M[a][b] = 0.0;
+      for (int u = 0; u < gamma; ++u) {
+        const int j = hi[u], t = hp[u];
+        if (j >= 0 && j < m && t >= 0 && t < delta && ps[j] > t) {
+          double x[ELL];
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) x[k] = Rs[k * m + j];
+#pragma unroll
+          for (int a = 0; a < ELL; ++a)
+#pragma unroll
+            for (int b = 0; b <= a; ++b) M[a][b] += x[a] * x[b];
+        }
+      }
+      cholesky<ELL>(M);
+      for (int u = 0; u < gamma; ++u) {
+        const int j = hi[u], t = hp[u];
+        if (!(j >= 0 && j < m && t >= 0 && t < delta)) continue;
+        float *dst = Bp + j * wstride + t * ELL;
+        if (ps[j] > t) {
+          double c[ELL];
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) c[k] = Rs[k * m + j];
+          chol_solve<ELL>(M, c);
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) dst[k] = float(c[k]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) dst[k] = 0.f;
+        }
+      }
+    } else {
+      // 0 < Delta < ell: collect the members (at most ell - 1 of them)
+      int selj[ELL], selt[ELL];
+#pragma unroll
+      for (int a = 0; a < ELL; ++a) selj[a] = selt[a] = -1;
+      int cnt = 0;
+      for (int u = 0; u < gamma; ++u) {
+        const int j = hi[u], t = hp[u];
+        if (!(j >= 0 && j < m && t >= 0 && t < delta)) continue;
+        if (ps[j] > t) {
+#pragma unroll
+          for (int a = 0; a < ELL; ++a)
+            if (a == cnt) {
+              selj[a] = j;
+              selt[a] = t;
+            }
+          ++cnt;
+        } else {
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
+        }
+      }
+      double X[ELL][ELL];  // X[k][a] = R[k][selj[a]], zero for a >= Delta
+#pragma unroll
+      for (int a = 0; a < ELL; ++a) {
+        const int ja = a < Delta ? selj[a] : 0;  // index stays in range even if speculated
+#pragma unroll
+        for (int k = 0; k < ELL; ++k) X[k][a] = a < Delta ? double(Rs[k * m + ja]) : 0.0;
+      }
+      double H[ELL][ELL];
+#pragma unroll
+      for (int a = 0; a < ELL; ++a)
+#pragma unroll
+        for (int b = 0; b <= a; ++b) {
+          double v = 0.0;
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) v += X[k][a] * X[k][b];
+          H[a][b] = (a < Delta) ? v : (a == b ? 1.0 : 0.0);
+        }
+      cholesky<ELL>(H);
+#pragma unroll
+      for (int a = 0; a < ELL; ++a) {
+        if (a >= Delta) break;
+        double z[ELL];  // column a of H^-1 (= row a, H symmetric)
+#pragma unroll
+        for (int b = 0; b < ELL; ++b) z[b] = (a == b) ? 1.0 : 0.0;
+        chol_solve<ELL>(H, z);
+        float *dst = Bp + selj[a] * wstride + selt[a] * ELL;
+#pragma unroll
+        for (int k = 0; k < ELL; ++k) {
+          double c = 0.0;
+#pragma unroll
+          for (int b = 0; b < ELL; ++b) c += z[b] * X[k][b];
+          dst[k] = float(c);
+        }
+      }
+    }
+  }
+
+  err = wave_sum(err);
+  const bool ok = __all(all_ok);
+  if (lane == 0) {
+    dec[p] = invalid ? GC_DEC_INVALID : (ok ? GC_DEC_YES : GC_DEC_NO);
+    coef_err[p] = err;
+  }
+}
+
+template <int ELL>
+void launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *order, int delta,
+                   const int32_t *holder, const int32_t *hpos, int gamma, const float *R,
+                   int32_t *cov, uint8_t *dec, int32_t *coef_err, float *Bc, hipStream_t st) {
+  const int64_t blocks = ceil_div(P, kDecodeWaves);
+  const size_t lds = sizeof(float) * ELL * m;
+  hipLaunchKernelGGL(decode_kernel<ELL>, dim3(unsigned(blocks)), dim3(kDecodeThreads), lds, st,
+                     psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc);
+}
+
+}  // namespace
+}  // namespace gcx
+
+extern "C" int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m,
+                                const int32_t *order, int32_t delta, const int32_t *holder,
+                                const int32_t *hpos, int32_t gamma, const float *R, int32_t ell,
+                                int32_t *cov, uint8_t *dec, int32_t *coef_err, float *Bc,
+                                hipStream_t stream) {
+  using namespace gcx;
+  if (P < 0 || N < 1 || m < 1 || m > GC_MAX_M || delta < 1 || delta > GC_MAX_DELTA ||
+      gamma < 1 || gamma > GC_MAX_DELTA || ell < 1 || ell > GC_MAX_ELL)
+    return GC_EINVAL;
+  if (P == 0) return GC_OK;
+  if (P > int64_t(kDecodeWaves) * 0x7fffffffLL) return GC_EINVAL;
+  if (!psi || !order || !holder || !hpos || !R || !cov || !dec || !coef_err || !Bc)
+    return GC_EINVAL;
+  const int dev = check_device();
+  if (dev != GC_OK) return dev;
+  (void)hipGetLastError();
+  switch (ell) {
+#define GC_CASE(E)                                                                              \
+  case E:                                                                                       \
+    launch_decode<E>(psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc, \
+                     stream);                                                                   \
+    break;
+    GC_CASE(1) GC_CASE(2) GC_CASE(3) GC_CASE(4) GC_CASE(5) GC_CASE(6) GC_CASE(7) GC_CASE(8)
+#undef GC_CASE
+    default: return GC_EINVAL;
+  }
+  return launch_status();
+}

@@ -1,0 +1,262 @@
+// gc_encode: every simulated worker's transmitted vector (Sec. 2, worker encode)
+//   T[p][j][x] = sum_{t < psi[p][j]} sum_{k < ell} Bc[p][j][t][k] * g_{order[j][t]}[k*L + x]
+//
+// Bandwidth design (HBM-bound on the T write, ~1 flop per byte):
+//   - a block owns one slice of W consecutive x positions and a contiguous
+//     range of rows r = p*m + j;  it stages the W-wide slice of every block k
+//     of every chunk gradient in LDS once (N*ell*W values, stored type), so
+//     the ~psi*ell reads per output element hit LDS, not HBM or L2;
+//   - per-row metadata (psi, the chunk indices and the coefficients of the
+//     row's processed prefix) is staged group by group in LDS with coalesced
+//     loads, then read back as wave-uniform broadcasts;
+//   - a wave writes one row segment of W floats (64 lanes x VEC floats)
+//     per row: fully coalesced, and every T byte is written exactly once;
+//   - block -> (slice, row range) is XCD-aware: blocks are dispatched
+//     round-robin over the 8 XCDs, and every block of a slice runs on the
+//     same XCD, so its L2 serves the repeated slice staging.
+#include "common.h"
+
+namespace gcx {
+namespace {
+
+constexpr int kEncThreads = 512;
+constexpr int kEncWaves = kEncThreads / kWave;
+constexpr size_t kEncSliceLds = 96 * 1024;   // G slice budget
+constexpr size_t kEncMetaLds = 24 * 1024;    // row metadata budget
+constexpr int64_t kEncRowsPerBlock = 4096;
+
+template <typename GT>
+__device__ __forceinline__ float to_f32(GT v);
+template <>
+__device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) { return bf16_to_f32(v); }
+
+template <typename GT, int VEC>
+struct Vec;
+template <>
+struct Vec<float, 4> { using T = float4; };
+template <>
+struct Vec<float, 2> { using T = float2; };
+template <>
+struct Vec<float, 1> { using T = float; };
+template <>
+struct Vec<uint16_t, 4> { using T = uint2; };
+template <>
+struct Vec<uint16_t, 2> { using T = uint32_t; };
+template <>
+struct Vec<uint16_t, 1> { using T = uint16_t; };
+
+template <typename GT, int VEC>
+__device__ __forceinline__ void load_vec(const GT *p, float (&v)[VEC]) {
+  using VT = typename Vec<GT, VEC>::T;
+  const VT raw = *reinterpret_cast<const VT *>(p);
+  const GT *e = reinterpret_cast<const GT *>(&raw);
+#pragma unroll
+  for (int q = 0; q < VEC; ++q) v[q] = to_f32<GT>(e[q]);
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_vec(float *p, const float (&v)[VEC]) {
+  if constexpr (VEC == 4) {
+    *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  } else if constexpr (VEC == 2) {
+    *reinterpret_cast<float2 *>(p) = make_float2(v[0], v[1]);
+  } else {
+    *p = v[0];
+  }
+}
+
+struct EncodeArgs {
+  const void *G;
+  int N;
+  int64_t d;
+  int64_t L;
+  const int32_t *psi;
+  const int32_t *order;
+  const float *Bc;
+  int64_t rows;  // P * m
+  int m;
+  int delta;
+  int ell;
+  float *T;
+  int nslices;
+  int64_t rows_per_block;
+  int group_rows;  // rows of metadata staged per step
+};
+
+// LDS layout: [ G slice : N*ell*W GT ][ psi : group ][ chunk : group*delta ][ coef : group*delta*ell ]
+// STAGE = false (the slice of every chunk does not fit in LDS): no slice in
+// LDS; the gradient values are read from global memory, where L2 holds the
+// slice for the block's many rows.
+template <typename GT, int VEC, bool STAGE>
+__global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
+  constexpr int W = kWave * VEC;
+  extern __shared__ __align__(16) unsigned char lds[];
+  GT *Gs = reinterpret_cast<GT *>(lds);
+  const size_t gbytes =
+      STAGE ? (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15) : size_t(0);
+  int32_t *mpsi = reinterpret_cast<int32_t *>(lds + gbytes);
+  int32_t *mchunk = mpsi + a.group_rows;
+  float *mcoef = reinterpret_cast<float *>(mchunk + size_t(a.group_rows) * a.delta);
+
+  // block -> (slice, row block); every block of a slice lands on one XCD
+  const int64_t b = blockIdx.x;
+  int64_t slice, rblock;
+  if ((a.nslices & 7) == 0) {
+    const int64_t per = a.nslices >> 3;
+    slice = (b & 7) + 8 * ((b >> 3) % per);
+    rblock = b / a.nslices;
+  } else {
+    slice = b % a.nslices;
+    rblock = b / a.nslices;
+  }
+  const int64_t x0 = slice * W;
+  const int64_t r0 = rblock * a.rows_per_block;
+  const int64_t r1 = r0 + a.rows_per_block < a.rows ? r0 + a.rows_per_block : a.rows;
+
+  // stage the slice: Gs[(c*ell + k)*W + w] = g_c[k*L + x0 + w] (zero past L or past d)
+  const GT *G = reinterpret_cast<const GT *>(a.G);
+  const int nrow = STAGE ? a.N * a.ell : 0;
+  for (int e = threadIdx.x; e < nrow * W; e += kEncThreads) {
+    const int ck = e / W, w = e % W;
+    const int c = ck / a.ell, k = ck % a.ell;
+    const int64_t x = x0 + w;
+    const int64_t col = int64_t(k) * a.L + x;
+    Gs[e] = (x < a.L && col < a.d) ? G[int64_t(c) * a.d + col] : GT(0);
+  }
+
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int stride_row = a.delta * a.ell;
+  const int64_t xl = x0 + int64_t(lane) * VEC;  // this lane's first x
+  for (int64_t g0 = r0; g0 < r1; g0 += a.group_rows) {
+    const int gn = int(r1 - g0 < a.group_rows ? r1 - g0 : a.group_rows);
+    __syncthreads();  // previous group fully consumed (and the slice staged)
+    for (int e = threadIdx.x; e < gn; e += kEncThreads) {
+      const int64_t r = g0 + e;
+      const int j = int(r % a.m);
+      int v = a.psi[r];
+      v = v < 0 ? 0 : (v > a.delta ? a.delta : v);
+      mpsi[e] = v;
+      for (int t = 0; t < a.delta; ++t) {
+        int c = a.order[int64_t(j) * a.delta + t];
+        mchunk[e * a.delta + t] = (c >= 0 && c < a.N) ? c : -1;
+      }
+    }
+    const float *src = a.Bc + g0 * stride_row;
+    for (int e = threadIdx.x; e < gn * stride_row; e += kEncThreads) mcoef[e] = src[e];
+    __syncthreads();
+
+    for (int e = wave; e < gn; e += kEncWaves) {
+      const int64_t r = g0 + e;
+      const int np = mpsi[e];
+      float acc[VEC];
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) acc[q] = 0.f;
+      for (int t = 0; t < np; ++t) {
+        const int c = mchunk[e * a.delta + t];
+        if (c < 0) continue;
+        for (int k = 0; k < a.ell; ++k) {
+          const float w = mcoef[e * stride_row + t * a.ell + k];
+          float g[VEC];
+          if constexpr (STAGE) {
+            load_vec<GT, VEC>(Gs + (size_t(c) * a.ell + k) * W + lane * VEC, g);
+          } else {
+            const int64_t col = int64_t(k) * a.L + xl;
+            if (xl < a.L && col < a.d) {
+              load_vec<GT, VEC>(G + int64_t(c) * a.d + col, g);
+            } else {
+#pragma unroll
+              for (int q = 0; q < VEC; ++q) g[q] = 0.f;
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < VEC; ++q) acc[q] = fmaf(w, g[q], acc[q]);
+        }
+      }
+      if (xl < a.L) store_vec<VEC>(a.T + r * a.L + xl, acc);
+    }
+  }
+}
+
+template <typename GT, int VEC, bool STAGE>
+int launch_encode(EncodeArgs a, hipStream_t st) {
+  constexpr int W = kWave * VEC;
+  a.nslices = int(ceil_div(a.L, W));
+  const size_t gbytes =
+      STAGE ? (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15) : size_t(0);
+  const size_t per_row = sizeof(int32_t) * (1 + a.delta) + sizeof(float) * a.delta * a.ell;
+  int group = int(kEncMetaLds / per_row);
+  if (group > 1024) group = 1024;
+  if (group < 1) group = 1;
+  a.group_rows = group;
+  a.rows_per_block = kEncRowsPerBlock;
+  const int64_t rblocks = ceil_div(a.rows, a.rows_per_block);
+  const int64_t blocks = rblocks * a.nslices;
+  if (blocks > 0x7fffffffLL) return GC_EINVAL;
+  const size_t lds = gbytes + per_row * group;
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_kernel<GT, VEC, STAGE>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
+    return GC_ELAUNCH;
+  hipLaunchKernelGGL((encode_kernel<GT, VEC, STAGE>), dim3(unsigned(blocks)), dim3(kEncThreads), lds,
+                     st, a);
+  return GC_OK;
+}
+
+template <typename GT>
+int dispatch_encode(const EncodeArgs &a, int vec, bool stage, hipStream_t st) {
+  if (stage) {
+    return vec == 4 ? launch_encode<GT, 4, true>(a, st)
+                    : (vec == 2 ? launch_encode<GT, 2, true>(a, st) : launch_encode<GT, 1, true>(a, st));
+  }
+  return vec == 4 ? launch_encode<GT, 4, false>(a, st)
+                  : (vec == 2 ? launch_encode<GT, 2, false>(a, st) : launch_encode<GT, 1, false>(a, st));
+}
+
+}  // namespace
+}  // namespace gcx
+
+extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_t *psi,
+                         const int32_t *order, const float *Bc, int64_t P, int32_t m,
+                         int32_t delta, int32_t ell, float *T, hipStream_t stream) {
+  using namespace gcx;
+  if (N < 1 || d < 1 || P < 0 || m < 1 || m > GC_MAX_M || delta < 1 || delta > GC_MAX_DELTA ||
+      ell < 1 || ell > GC_MAX_ELL || (g_dtype != GC_F32 && g_dtype != GC_BF16))
+    return GC_EINVAL;
+  if (P == 0) return GC_OK;
+  if (!G || !psi || !order || !Bc || !T) return GC_EINVAL;
+  const int dev = check_device();
+  if (dev != GC_OK) return dev;
+  EncodeArgs a{};
+  a.G = G;
+  a.N = N;
+  a.d = d;
+  a.L = ceil_div(d, ell);
+  a.psi = psi;
+  a.order = order;
+  a.Bc = Bc;
+  a.rows = P * m;
+  a.m = m;
+  a.delta = delta;
+  a.ell = ell;
+  a.T = T;
+  // widest vector the row length and the alignment of T allow; stage the
+  // slice of every chunk in LDS when it fits, else read G through L2
+  const size_t esize = g_dtype == GC_F32 ? 4 : 2;
+  const uintptr_t ta = reinterpret_cast<uintptr_t>(T), ga = reinterpret_cast<uintptr_t>(G);
+  int vec = (a.L % 4 == 0 && (ta & 15) == 0) ? 4 : ((a.L % 2 == 0 && (ta & 7) == 0) ? 2 : 1);
+  int svec = vec;
+  while (svec > 1 && size_t(N) * ell * kWave * svec * esize > kEncSliceLds) svec >>= 1;
+  const bool stage = size_t(N) * ell * kWave * svec * esize <= kEncSliceLds;
+  if (stage) {
+    vec = svec;
+  } else {
+    // direct vector loads of G need d and the base to be multiples of the vector
+    while (vec > 1 && (d % vec != 0 || (ga & (size_t(vec) * esize - 1)) != 0)) vec >>= 1;
+  }
+  (void)hipGetLastError();
+  const int st = g_dtype == GC_F32 ? dispatch_encode<float>(a, vec, stage, stream)
+                                   : dispatch_encode<uint16_t>(a, vec, stage, stream);
+  if (st != GC_OK) return st;
+  return launch_status();
+}

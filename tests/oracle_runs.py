@@ -1,0 +1,110 @@
+"""Batched drivers around the oracle for the parity tests (test infrastructure).
+
+Loops the per-pattern oracle functions over many patterns and computes the
+forward-error bounds the GPU results are held to.  Uses only ``oracle`` and
+``workloads``.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle.assignment as OA
+import oracle.gradients as OG
+import oracle.protocol as OP
+
+U = 2.0 ** -24          # unit roundoff of fp32 (round to nearest)
+
+
+def gamma(n):
+    """gamma_n = n u / (1 - n u): the classical bound factor for n fp32 roundings."""
+    n = np.asarray(n, dtype=np.float64)
+    return n * U / (1.0 - n * U)
+
+
+def coverage_all(O, psi):
+    """cov [P][N], dec [P] (for each ell given later), via the oracle per pattern."""
+    return np.stack([OP.coverage(O, p) for p in psi]).astype(np.int64)
+
+
+def coefficients(O, psi, R, per_worker=False):
+    """Bc [P][m][delta][ell] fp64 and the per-(pattern, chunk) 2-norm condition numbers
+    of R[:, S_i] (0 where Delta_i = 0)."""
+    R = np.asarray(R, dtype=np.float64)
+    ell = R.shape[0]
+    N, m = O.shape
+    Bcs, kappas = [], []
+    for p in psi:
+        B = OP.encoding_matrix(O, p, R) if per_worker else OP.encoding_matrix_per_chunk(O, p, R)
+        Bcs.append(OP.compact(B, O, ell))
+        kap = np.zeros(N)
+        for i, S in enumerate(OP.processed_sets(O, p)):
+            if len(S):
+                kap[i] = np.linalg.cond(R[:, S])
+        kappas.append(kap)
+    return np.stack(Bcs), np.stack(kappas)
+
+
+def bc_bound(Bc_ref, kappa, O):
+    """Elementwise bound for the GPU's Bc: one fp32 rounding of the fp64 value plus the
+    fp64 Gram/Cholesky solve's error, which grows like kappa^2 * 2^-53 times the block's size."""
+    order, _, _ = OA.tables(O)
+    P, m, delta, ell = Bc_ref.shape
+    out = 2 * U * np.abs(Bc_ref)
+    for p in range(P):
+        for j in range(m):
+            for t in range(delta):
+                i = order[j, t]
+                if i < 0:
+                    continue
+                out[p, j, t, :] += 1e-14 * max(1.0, kappa[p, i]) ** 2 * (np.abs(Bc_ref[p, j, t, :]).max() + 1e-300)
+    return out
+
+
+def gblocks(G, ell):
+    return OP.blocks(np.asarray(G, dtype=np.float64), ell)       # [N][ell][L]
+
+
+def encode_ref(Bc, psi, order, G, ell):
+    """T [P][m][L] from compact coefficients over each worker's processed prefix (fp64),
+    and its magnitude sum_{t,k} |Bc||g| for the error bound."""
+    Gb = gblocks(G, ell)
+    N, _, L = Gb.shape
+    P, m, delta, _ = Bc.shape
+    T = np.zeros((P, m, L))
+    M = np.zeros((P, m, L))
+    n_terms = np.zeros((P, m))
+    for p in range(P):
+        for j in range(m):
+            npj = min(max(int(psi[p, j]), 0), delta)
+            for t in range(npj):
+                c = order[j, t]
+                if c < 0:
+                    continue
+                for k in range(ell):
+                    T[p, j] += Bc[p, j, t, k] * Gb[c, k]
+                    M[p, j] += abs(Bc[p, j, t, k]) * np.abs(Gb[c, k])
+                    n_terms[p, j] += 1
+    return T, M, n_terms
+
+
+def reconstruct_ref(T, R, d):
+    R = np.asarray(R, dtype=np.float64)
+    P, m, L = T.shape
+    gh = np.einsum("km,pml->pkl", R, T).reshape(P, -1)[:, :d]
+    mag = np.einsum("km,pml->pkl", np.abs(R), np.abs(T)).reshape(P, -1)[:, :d]
+    return gh, mag
+
+
+def end_to_end(O, psi, R, G, per_worker=False):
+    """Full oracle: coefficients from psi and R, encode, combine.  Returns ghat [P][d]."""
+    R = np.asarray(R, dtype=np.float64)
+    G = np.asarray(G, dtype=np.float64)
+    out = []
+    for p in psi:
+        B = OP.encoding_matrix(O, p, R) if per_worker else OP.encoding_matrix_per_chunk(O, p, R)
+        out.append(OP.reconstruct(OP.encode(B, G, R.shape[0]), R, G.shape[1]))
+    return np.stack(out)
+
+
+def chunk_grads(X, y, W, loss):
+    return OG.chunk_gradients(X, y, W, loss)

@@ -1,0 +1,118 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and its
+host-only entry points and host-side validation behave as documented."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle.assignment as OA
+from paper_2405_19509_amd import gcx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gcx.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gc_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_hot_path():
+    syms = declared_symbols()
+    for name in ("gc_assign", "gc_chunk_grads", "gc_encode", "gc_decode_coeffs", "gc_reconstruct"):
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol():
+    lib = gcx.load()
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+    assert set(declared_symbols()) == set(gcx.SIGNATURES)
+
+
+def test_version_and_strerror():
+    assert gcx.gc_version() >= 100
+    for st in (gcx.GC_OK, gcx.GC_EINVAL, gcx.GC_ELAUNCH, gcx.GC_ENOTSUP, 7):
+        assert isinstance(gcx.strerror(st), str)
+
+
+@pytest.mark.parametrize("m,s", [(1, 0), (3, 1), (6, 2), (20, 3), (50, 4), (100, 9), (200, 19), (9, 8)])
+def test_assign_cyclic_matches_oracle(m, s):
+    O, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, m, m, s)
+    assert (O == OA.cyclic_O(m, m, s)).all()
+    o2, h2, p2 = OA.tables(OA.cyclic_O(m, m, s))
+    assert (order == o2).all() and (holder == h2).all() and (hpos == p2).all()
+
+
+def test_assign_from_order_matches_oracle():
+    g = np.random.default_rng(0)
+    for _ in range(30):
+        N, m = g.integers(1, 12, size=2)
+        A = g.random((N, m)) < 0.4
+        O = np.zeros((N, m), dtype=np.int32)
+        for j in range(m):
+            rows = np.flatnonzero(A[:, j])
+            g.shuffle(rows)
+            O[rows, j] = np.arange(1, len(rows) + 1)
+        delta = max(1, int((O != 0).sum(axis=0).max()))
+        gamma = max(1, int((O != 0).sum(axis=1).max()))
+        _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, N, m, -1, O, delta, gamma)
+        o2, h2, p2 = OA.tables(O, delta, gamma)
+        assert (order == o2).all() and (holder == h2).all() and (hpos == p2).all()
+
+
+def _raw_assign(kind, N, m, s, O, delta, gamma):
+    lib = gcx.load()
+    order = np.zeros((m, max(delta, 1)), dtype=np.int32)
+    holder = np.zeros((N, max(gamma, 1)), dtype=np.int32)
+    hpos = np.zeros((N, max(gamma, 1)), dtype=np.int32)
+    Op = O.ctypes.data if O is not None else None
+    return lib.gc_assign(kind, N, m, s, Op, delta, gamma, order.ctypes.data, holder.ctypes.data,
+                         hpos.ctypes.data)
+
+
+def test_assign_rejects_bad_arguments():
+    E = gcx.GC_EINVAL
+    assert _raw_assign(gcx.GC_ASSIGN_CYCLIC, 5, 6, 1, None, 2, 2) == E      # N != m
+    assert _raw_assign(gcx.GC_ASSIGN_CYCLIC, 5, 5, 5, None, 6, 6) == E      # s >= m
+    assert _raw_assign(gcx.GC_ASSIGN_CYCLIC, 5, 5, 1, None, 3, 2) == E      # delta != s+1
+    assert _raw_assign(7, 5, 5, 1, None, 2, 2) == E                          # unknown kind
+    assert _raw_assign(gcx.GC_ASSIGN_ORDER, 3, 3, -1, None, 2, 2) == E       # O missing
+    bad = np.array([[1, 0, 0], [1, 0, 0], [0, 0, 0]], dtype=np.int32)      # two chunks at position 1
+    assert _raw_assign(gcx.GC_ASSIGN_ORDER, 3, 3, -1, bad, 3, 3) == E
+    gap = np.array([[1, 0, 0], [3, 0, 0], [0, 0, 0]], dtype=np.int32)      # positions 1, 3: a gap
+    assert _raw_assign(gcx.GC_ASSIGN_ORDER, 3, 3, -1, gap, 3, 3) == E
+    narrow = np.array([[1, 1, 1], [0, 0, 0], [0, 0, 0]], dtype=np.int32)   # gamma 3 > table width 2
+    assert _raw_assign(gcx.GC_ASSIGN_ORDER, 3, 3, -1, narrow, 1, 2) == E
+
+
+def test_device_calls_validate_on_the_host():
+    """Bad sizes and null pointers are rejected before any device work (no GPU needed)."""
+    lib = gcx.load()
+    E = gcx.GC_EINVAL
+    p = 16  # a dummy non-null address; validation must fail before it is used
+    assert lib.gc_decode_coeffs(p, 4, 6, 0, p, 3, p, p, 3, p, 1, p, p, p, p, None) == E       # m = 0
+    assert lib.gc_decode_coeffs(p, 4, 6, 6, p, 3, p, p, 3, p, 9, p, p, p, p, None) == E       # ell > 8
+    assert lib.gc_decode_coeffs(None, 4, 6, 6, p, 3, p, p, 3, p, 1, p, p, p, p, None) == E    # null psi
+    assert lib.gc_decode_coeffs(p, 4, 6, 2000, p, 3, p, p, 3, p, 1, p, p, p, p, None) == E    # m too big
+    assert lib.gc_decode_coeffs(p, -1, 6, 6, p, 3, p, p, 3, p, 1, p, p, p, p, None) == E      # P < 0
+    assert lib.gc_decode_coeffs(p, 0, 6, 6, p, 3, p, p, 3, p, 1, p, p, p, p, None) == gcx.GC_OK  # P = 0
+    assert lib.gc_encode(p, 5, 6, 64, p, p, p, 4, 6, 3, 1, p, None) == E                       # dtype
+    assert lib.gc_encode(p, 0, 6, 0, p, p, p, 4, 6, 3, 1, p, None) == E                        # d = 0
+    assert lib.gc_encode(None, 0, 6, 64, p, p, p, 4, 6, 3, 1, p, None) == E                    # null G
+    assert lib.gc_encode(p, 0, 6, 64, p, p, p, 0, 6, 3, 1, p, None) == gcx.GC_OK                # P = 0
+    assert lib.gc_reconstruct(p, p, 4, 6, 64, 0, p, None, None, None, 0, None) == E            # ell = 0
+    assert lib.gc_reconstruct(p, p, 4, 6, 64, 1, p, None, p, None, 0, None) == E               # sqerr w/o gsum
+    assert lib.gc_reconstruct(p, p, 4, 6, 1 << 20, 1, None, p, p, None, 0, None) == E          # workspace
+    assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 5, p, p, 1 << 20, None) == E                # loss
+    assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 0, p, p, 4, None) == E                      # small ws
+    assert lib.gc_sum_chunks(p, 3, 2, 8, p, None) == E
+
+
+def test_workspace_sizes():
+    assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 1) == 4 * 50 * 512
+    assert gcx.gc_reconstruct_workspace_size(10000, 50, 16384, 1) == 8 * 10000 * 4
+    assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 1) == 0
+    assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 32

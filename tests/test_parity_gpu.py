@@ -1,0 +1,302 @@
+"""GPU parity: every C-ABI call against the oracle on identical seeded inputs.
+
+Stage by stage, each call receives inputs that come from the generators or
+from the oracle (never from another GPU call) and is compared element by
+element with the oracle:
+  - coverage, decodability and coefficient error: bit-exact;
+  - Bc: one fp32 rounding plus the fp64 solve's kappa^2 * 2^-53 error;
+  - T and the estimate: the classical fp32 summation bound gamma_n * sum |terms|;
+  - end to end: relative L2 error of the estimate <= 1e-5 at ell = 1, and the
+    cancellation-aware bound at ell >= 2.
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+
+import numpy as np
+import pytest
+
+import oracle.assignment as OA
+import oracle.protocol as OP
+import oracle_runs as R_
+from workloads import BANDWIDTH, HEADLINE, LARGE, SMALL, TINY, Workload, gen
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2405_19509_amd import gcx  # noqa: E402
+
+U = R_.U
+
+# ragged shapes: N > 64 lanes, d not a multiple of 4 / of ell, pattern counts not multiples of tiles
+RAGGED = Workload(name="ragged_m70_d1001", N=70, m=70, s=5, d=1001, P=37, ells=(1, 3),
+                  g_dtype="f32", pattern="uniform", forced_zero=7)
+RAGGED_BF16 = dataclasses.replace(RAGGED, name="ragged_m70_d1000_bf16", d=1000, g_dtype="bf16")
+LARGE_D16 = dataclasses.replace(LARGE, name="given_m200_d65536_bf16", d=1 << 16)
+BANDWIDTH_D16 = dataclasses.replace(BANDWIDTH, name="given_m100_d65536", d=1 << 16)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+@functools.lru_cache(maxsize=None)
+def tables(wl: Workload):
+    O, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, wl.N, wl.m, wl.s)
+    assert (O == OA.cyclic_O(wl.N, wl.m, wl.s)).all()
+    return O.astype(np.int64), order, holder, hpos
+
+
+@functools.lru_cache(maxsize=None)
+def patterns(wl: Workload, count: int, variant: str = "exact"):
+    return gen.psi(wl, count=min(count, wl.P), variant=variant)
+
+
+@functools.lru_cache(maxsize=None)
+def given_G(wl: Workload):
+    return gen.given_G(wl)
+
+
+def G_torch(wl, G):
+    if wl.g_dtype == "bf16":
+        return dev(G.view(np.int16)).view(torch.bfloat16)
+    return dev(G)
+
+
+def run_decode(wl, psi, R):
+    O, order, holder, hpos = tables(wl)
+    cov, dec, cerr, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+    return host(cov), host(dec), host(cerr), host(Bc)
+
+
+def check_decode(wl, psi, R, per_worker=False):
+    O, order, _, _ = tables(wl)
+    ell = R.shape[0]
+    cov, dec, cerr, Bc = run_decode(wl, psi, R)
+    cov_ref = R_.coverage_all(O, psi)
+    assert (cov == cov_ref).all()
+    dec_ref = np.array([OP.decodable(O, p, ell) for p in psi])
+    assert (dec == dec_ref.astype(np.uint8)).all()
+    cerr_ref = np.array([OP.coef_err(O, p, ell) for p in psi])
+    assert (cerr == cerr_ref).all()
+    Bc_ref, kappa = R_.coefficients(O, psi, R, per_worker=per_worker)
+    bound = R_.bc_bound(Bc_ref, kappa, O)
+    diff = np.abs(Bc.astype(np.float64) - Bc_ref)
+    worst = np.unravel_index(np.argmax(diff - bound), diff.shape)
+    assert (diff <= bound).all(), f"Bc off at {worst}: {Bc[worst]} vs {Bc_ref[worst]} (bound {bound[worst]})"
+    return Bc_ref, kappa
+
+
+DECODE_CASES = [
+    (TINY, 1, 100, True), (TINY, 2, 100, True), (TINY, 3, 100, True),
+    (SMALL, 1, 1000, False), (SMALL, 2, 1000, False), (SMALL, 2, 60, True),
+    (HEADLINE, 1, 400, False), (HEADLINE, 2, 400, False),
+    (BANDWIDTH, 1, 60, False), (BANDWIDTH, 2, 60, False), (BANDWIDTH, 8, 60, False),
+    (LARGE, 1, 12, False), (LARGE, 2, 12, False),
+    (RAGGED, 1, 37, True), (RAGGED, 3, 37, False), (RAGGED, 7, 37, False),
+]
+
+
+@pytest.mark.parametrize("wl,ell,count,per_worker", DECODE_CASES,
+                         ids=[f"{w.name}-l{e}-P{c}" for w, e, c, _ in DECODE_CASES])
+def test_decode_parity(wl, ell, count, per_worker):
+    psi = patterns(wl, count)
+    R = gen.shared_R(wl.m, ell)
+    check_decode(wl, psi, R, per_worker=per_worker)
+
+
+@pytest.mark.parametrize("ell", [1, 2, 4])
+def test_decode_parity_large_least_squares(ell):
+    psi = patterns(LARGE, 12, "ls")
+    assert (psi == 0).sum(axis=1).min() >= LARGE.ls_forced_zero
+    check_decode(LARGE, psi, gen.shared_R(LARGE.m, ell))
+
+
+def test_decode_edge_patterns():
+    """No worker done, all done, single worker done, s = 0, P not a multiple of 4."""
+    wl = dataclasses.replace(TINY, name="tiny_edges")
+    m, delta = wl.m, wl.delta
+    psi = np.array([[0] * m, [delta] * m, [delta] + [0] * (m - 1), [1] * m, [delta - 1] * m],
+                   dtype=np.int32)
+    for ell in (1, 2, 3, 8):
+        check_decode(wl, psi, gen.shared_R(m, ell), per_worker=True)
+    wl0 = Workload(name="s0", N=9, m=9, s=0, d=16, P=3, ells=(1,), pattern="uniform")
+    for ell in (1, 2):
+        check_decode(wl0, patterns(wl0, 3), gen.shared_R(9, ell), per_worker=True)
+
+
+def test_decode_invalid_psi():
+    wl = TINY
+    psi = patterns(wl, 10).copy()
+    psi[3, 2] = wl.delta + 1
+    psi[7, 0] = -1
+    cov, dec, cerr, Bc = run_decode(wl, psi, gen.shared_R(wl.m, 2))
+    assert dec[3] == gcx.GC_DEC_INVALID and dec[7] == gcx.GC_DEC_INVALID
+    assert (Bc[3] == 0).all() and (Bc[7] == 0).all()
+    ok = [p for p in range(10) if p not in (3, 7)]
+    check_decode(wl, psi[ok], gen.shared_R(wl.m, 2))
+
+
+def test_decode_explicit_order_sec2_2():
+    """The non-cyclic example of Sec. 2.2 through GC_ASSIGN_ORDER: supports and coefficients."""
+    import pins
+    O = pins.sec2_2_O()
+    _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, 5, 5, -1, O)
+    R = gen.shared_R(5, 2)
+    for psi_row, golden in (([5, 2, 0, 2, 3], "sec2_2_support_exact.txt"),
+                            ([4, 2, 0, 2, 3], "sec2_2_support_approx.txt")):
+        psi = np.array([psi_row], dtype=np.int32)
+        cov, dec, cerr, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+        cov, dec, cerr, Bc = host(cov), host(dec), host(cerr), host(Bc)
+        assert (cov[0] == OP.coverage(O, psi[0])).all()
+        assert cerr[0] == OP.coef_err(O, psi[0], 2)
+        B_ref = OP.encoding_matrix(O, psi[0], R)
+        Bc_ref = OP.compact(B_ref, O, 2)
+        assert np.allclose(Bc[0], Bc_ref, rtol=4 * U, atol=1e-6)
+        # the support of B rebuilt from Bc is the printed one
+        supp = np.zeros((5, 10), dtype=bool)
+        for j in range(5):
+            for t in range(order.shape[1]):
+                i = order[j, t]
+                if i >= 0:
+                    supp[j, 2 * i:2 * i + 2] = Bc[0, j, t] != 0
+        assert (supp == np.array(pins.load_rows(golden), dtype=bool)).all()
+
+
+# ---------------------------------------------------------------------------
+# encode and combine, stage by stage on oracle-made inputs
+# ---------------------------------------------------------------------------
+
+ENC_CASES = [
+    (TINY, 1, 100), (TINY, 2, 100), (TINY, 3, 100),
+    (SMALL, 1, 40), (SMALL, 2, 40),
+    (HEADLINE, 1, 12), (HEADLINE, 2, 12),
+    (BANDWIDTH_D16, 1, 6), (BANDWIDTH_D16, 8, 6),
+    (LARGE_D16, 1, 3), (LARGE_D16, 2, 3),
+    (RAGGED, 1, 37), (RAGGED, 3, 37), (RAGGED_BF16, 3, 37),
+]
+
+
+def _data_G(wl):
+    if wl.n is not None:
+        X, y, w = gen.regression_data(wl)
+        return R_.chunk_grads(X, y, w, wl.loss).astype(np.float32)
+    return given_G(wl)
+
+
+@pytest.mark.parametrize("wl,ell,count", ENC_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in ENC_CASES])
+def test_encode_and_reconstruct_parity(wl, ell, count):
+    O, order, holder, hpos = tables(wl)
+    psi = patterns(wl, count)
+    R = gen.shared_R(wl.m, ell)
+    Bc_ref, _ = R_.coefficients(O, psi, R)
+    Bc32 = Bc_ref.astype(np.float32)
+    G = _data_G(wl)
+    Gw = OP.widen(G, wl.g_dtype)
+    # encode on identical inputs: G, psi and the oracle's coefficients rounded to fp32
+    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32)))
+    T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, Gw, ell)
+    bound = R_.gamma(nterm)[:, :, None] * M
+    diff = np.abs(T.astype(np.float64) - T_ref)
+    assert (diff <= bound).all(), f"T off by {np.max(diff - bound)}"
+    assert (T[psi == 0] == 0).all()
+    # combine on identical inputs: the oracle's T rounded to fp32
+    T32 = T_ref.astype(np.float32)
+    gsum_ref = Gw.sum(axis=0)
+    gsum32 = gsum_ref.astype(np.float32)
+    ghat, sqerr = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, gsum=dev(gsum32))
+    ghat, sqerr = host(ghat), host(sqerr)
+    gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, wl.d)
+    gb = R_.gamma(wl.m) * mag
+    gdiff = np.abs(ghat.astype(np.float64) - gh_ref)
+    assert (gdiff <= gb).all(), f"ghat off by {np.max(gdiff - gb)}"
+    se_ref = ((gh_ref - gsum32.astype(np.float64)) ** 2).sum(axis=1)
+    E = np.sqrt((gb ** 2).sum(axis=1))
+    assert (np.abs(sqerr - se_ref) <= 2 * np.sqrt(se_ref) * E + E * E + 1e-12 * se_ref).all()
+    # error-only mode gives the same sqerr
+    _, sq2 = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, gsum=dev(gsum32), want_ghat=False)
+    assert (host(sq2) == sqerr).all()
+
+
+def test_sum_chunks():
+    for wl in (TINY, RAGGED, RAGGED_BF16, LARGE_D16):
+        G = _data_G(wl)
+        Gw = OP.widen(G, wl.g_dtype)
+        gs = host(gcx.gc_sum_chunks(G_torch(wl, G))).astype(np.float64)
+        want = Gw.sum(axis=0)
+        assert (np.abs(gs - want) <= 2 * U * np.abs(want) + 1e-30).all()
+
+
+# ---------------------------------------------------------------------------
+# chunk gradients
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wl", [TINY, SMALL, HEADLINE], ids=lambda w: w.name)
+def test_chunk_grads_parity(wl):
+    X, y, w = gen.regression_data(wl)
+    G = host(gcx.gc_chunk_grads(dev(X), dev(y), dev(w), 0 if wl.loss == "linear" else 1))
+    G_ref = R_.chunk_grads(X, y, w, wl.loss)
+    rel = np.linalg.norm(G - G_ref, axis=1) / np.linalg.norm(G_ref, axis=1)
+    assert rel.max() <= 1e-5, rel.max()
+
+
+def test_chunk_grads_multi_point_and_ragged():
+    wl = Workload(name="ragged_reg", N=5, m=5, s=1, d=1001, P=1, ells=(1,), n=37, loss="logistic",
+                  x_std=0.05, w_std=0.1)
+    X, y, _ = gen.regression_data(wl)
+    W = gen.eval_points(wl, 3)
+    G = host(gcx.gc_chunk_grads(dev(X), dev(y), dev(W), gcx.GC_LOSS_LOGISTIC))
+    G_ref = R_.chunk_grads(X, y, W, "logistic")
+    rel = np.linalg.norm(G - G_ref, axis=-1) / np.linalg.norm(G_ref, axis=-1)
+    assert G.shape == (3, 5, 1001) and rel.max() <= 1e-5
+
+
+# ---------------------------------------------------------------------------
+# end to end: GPU pipeline vs full oracle
+# ---------------------------------------------------------------------------
+
+E2E_CASES = [(TINY, 1, 100), (TINY, 2, 100), (TINY, 3, 100), (SMALL, 1, 100), (SMALL, 2, 100),
+             (HEADLINE, 1, 40), (HEADLINE, 2, 40), (RAGGED, 1, 37), (RAGGED, 3, 37)]
+
+
+@pytest.mark.parametrize("wl,ell,count", E2E_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in E2E_CASES])
+def test_end_to_end(wl, ell, count):
+    O, order, holder, hpos = tables(wl)
+    psi = patterns(wl, count)
+    R = gen.shared_R(wl.m, ell)
+    if wl.n is not None:
+        X, y, w = gen.regression_data(wl)
+        Gd = gcx.gc_chunk_grads(dev(X), dev(y), dev(w), 0 if wl.loss == "linear" else 1)
+        G_ref = R_.chunk_grads(X, y, w, wl.loss)
+    else:
+        G = given_G(wl)
+        Gd = G_torch(wl, G)
+        G_ref = OP.widen(G, wl.g_dtype)
+    gsum = gcx.gc_sum_chunks(Gd)
+    _, _, _, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+    T = gcx.gc_encode(Gd, dev(psi), dev(order), Bc)
+    ghat, sqerr = gcx.gc_reconstruct(T, dev(R), wl.d, gsum=gsum)
+    ghat, sqerr = host(ghat).astype(np.float64), host(sqerr)
+    gh_ref = R_.end_to_end(O, psi, R, G_ref)
+    rel = np.linalg.norm(ghat - gh_ref, axis=1) / np.maximum(np.linalg.norm(gh_ref, axis=1), 1e-300)
+    if ell == 1:
+        assert rel.max() <= 1e-5, rel.max()
+    else:
+        # cancellation-aware bound: the combine's inputs are as large as sum_j |R||T_j|
+        Bc_ref, kappa = R_.coefficients(O, psi, R)
+        T_ref, M, nterm = R_.encode_ref(Bc_ref, psi, order, G_ref, ell)
+        _, mag = R_.reconstruct_ref(np.abs(T_ref) + M, R, wl.d)
+        allowed = np.maximum(1e-5, 4 * R_.gamma(wl.m + ell * wl.delta + 2) *
+                             np.linalg.norm(mag, axis=1) / np.maximum(np.linalg.norm(gh_ref, axis=1), 1e-300))
+        assert (rel <= allowed).all(), (rel / allowed).max()
+        well = kappa.max(axis=1) <= 100
+        if well.any():
+            print(f"ell={ell}: rel-L2 max {rel[well].max():.2e} over {well.sum()} patterns with kappa <= 100")
+    se_ref = ((ghat - G_ref.sum(axis=0)) ** 2).sum(axis=1)
+    assert np.allclose(sqerr, se_ref, rtol=1e-4, atol=1e-10 * float((G_ref.sum(axis=0) ** 2).sum()))
