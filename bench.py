@@ -1,0 +1,218 @@
+"""Throughput of the partial-straggler gradient-coding hot path on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic input:
+the chunk gradients of all N chunks (logistic regression, n samples each),
+their sum (the exact target), the coefficient solves for every straggler
+pattern, every simulated worker's encode, and the PS combine with the fused
+squared error against the exact target.  Workload: m = N = 50 workers,
+cyclic assignment with s = 4, d = 16384, n = 512, 10,000 straggler patterns
+(20% full stragglers, the rest uniform partial progress), ell = 1.
+
+    python bench.py [--steps K] [--warmup W] [--ell L] [--no-cpu-baseline]
+
+Prints one JSON line.  value = patterns decoded per second, whole job, with
+every input resident in HBM before the timed region starts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "straggler patterns decoded/sec at m=50,d=16384; HBM GB/s and MFMA % of peak"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--ell", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=1024,
+                    help="size of a plain device copy run once before warm-up (counter calibration)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(wl, ell, P):
+    """Compulsory bytes per launch: every input read once, every output written once."""
+    m, N, d, delta = wl.m, wl.N, wl.d, wl.delta
+    L = -(-d // ell)
+    enc = 4 * P * m * L + 4 * N * d + 4 * P * m + 4 * P * m * delta * ell + 4 * m * delta
+    rec = 4 * P * m * L + 4 * P * d + 4 * ell * m + 4 * d + 8 * P
+    dcd = 4 * P * m + 4 * P * N + P + 4 * P + 4 * P * m * delta * ell + 4 * ell * m + 12 * N * delta
+    grads = 4 * N * wl.n * wl.d + 4 * N * wl.n + 4 * d + 4 * N * d
+    return {"gc_encode": enc, "gc_reconstruct": rec, "gc_decode_coeffs": dcd, "gc_chunk_grads": grads,
+            "gc_sum_chunks": 4 * N * d + 4 * d}
+
+
+def cpu_baseline(wl, ell, X, y, w, psi, R, budget_s):
+    """The oracle as it stands, timed on this host on a bounded sample of the same workload."""
+    import oracle.assignment as OA
+    import oracle.gradients as OG
+    import oracle.protocol as OP
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    O = OA.cyclic_O(wl.N, wl.m, wl.s)
+    nchunk = 5
+    t0 = time.perf_counter()
+    G5 = OG.chunk_gradients(X[:nchunk], y[:nchunk], w, wl.loss)
+    t_grads = (time.perf_counter() - t0) * wl.N / nchunk
+    # the remaining chunk gradients are stood in for by the first ones' (only values differ)
+    G = np.concatenate([G5] * (wl.N // nchunk))
+    Rd = R.astype(np.float64)
+    t0 = time.perf_counter()
+    count = 0
+    while count < 20 or (time.perf_counter() - t0 < budget_s and count < wl.P):
+        p = psi[count]
+        B = OP.encoding_matrix(O, p, Rd)
+        T = OP.encode(B, G, ell)
+        OP.reconstruct(T, Rd, wl.d)
+        count += 1
+    t_pat = (time.perf_counter() - t0) / count
+    step = t_grads + wl.P * t_pat
+    return {
+        "value": wl.P / step, "unit": "patterns/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"chunk gradients of {nchunk}/{wl.N} chunks (time scaled to {wl.N}); "
+                   f"{count}/{wl.P} patterns through Algorithm 1 (per-worker min-norm lstsq), "
+                   f"encode and combine; per-step time = grads + P * per-pattern"),
+        "seconds_per_pattern": t_pat, "seconds_chunk_grads": t_grads,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (the hot path is one GPU's share; got --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2405_19509_amd import gcx
+    from workloads import HEADLINE, gen
+
+    gcx.load()  # fail loudly if the HIP library is missing
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    wl, ell, P = HEADLINE, args.ell, HEADLINE.P
+    dev = torch.device("cuda:0")
+
+    # ---- inputs (host generation, then resident in HBM) ----
+    X, y, w = gen.regression_data(wl)
+    psi = gen.psi(wl)
+    R = gen.shared_R(wl.m, ell)
+    O, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, wl.N, wl.m, wl.s)
+
+    def d(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    Xd, yd, wd, psid, Rd = d(X), d(y), d(w), d(psi), d(R)
+    orderd, holderd, hposd = d(order), d(holder), d(hpos)
+    L = -(-wl.d // ell)
+    G = torch.empty((wl.N, wl.d), dtype=torch.float32, device=dev)
+    gsum = torch.empty(wl.d, dtype=torch.float32, device=dev)
+    ws_g = torch.empty(gcx.gc_chunk_grads_workspace_size(wl.N, wl.n, wl.d, 1), dtype=torch.uint8, device=dev)
+    cov = torch.empty((P, wl.N), dtype=torch.int32, device=dev)
+    dec = torch.empty(P, dtype=torch.uint8, device=dev)
+    cerr = torch.empty(P, dtype=torch.int32, device=dev)
+    Bc = torch.empty((P, wl.m, wl.delta, ell), dtype=torch.float32, device=dev)
+    T = torch.empty((P, wl.m, L), dtype=torch.float32, device=dev)
+    ghat = torch.empty((P, wl.d), dtype=torch.float32, device=dev)
+    sqerr = torch.empty(P, dtype=torch.float64, device=dev)
+    ws_r = torch.empty(max(1, gcx.gc_reconstruct_workspace_size(P, wl.m, wl.d, ell)), dtype=torch.uint8,
+                       device=dev)
+    torch.cuda.synchronize()
+
+    names = ["gc_chunk_grads", "gc_sum_chunks", "gc_decode_coeffs", "gc_encode", "gc_reconstruct"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        gcx.gc_chunk_grads(Xd, yd, wd, gcx.GC_LOSS_LOGISTIC, G=G, workspace=ws_g)
+        mark(1)
+        gcx.gc_sum_chunks(G, gsum=gsum)
+        mark(2)
+        gcx.gc_decode_coeffs(psid, orderd, holderd, hposd, Rd, cov=cov, dec=dec, coef_err=cerr, Bc=Bc)
+        mark(3)
+        gcx.gc_encode(G, psid, orderd, Bc, T=T)
+        mark(4)
+        gcx.gc_reconstruct(T, Rd, wl.d, ghat=ghat, gsum=gsum, sqerr=sqerr, workspace=ws_r)
+        mark(5)
+
+    # a plain copy of known size, for calibrating HBM byte counters
+    if args.copy_probe_mib > 0:
+        nb = args.copy_probe_mib << 20
+        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps ----
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    per = {n: [] for n in names}
+    for ev in evs:
+        for i, n in enumerate(names):
+            per[n].append(ev[i].elapsed_time(ev[i + 1]))
+    avg_ms = {n: float(np.mean(v)) for n, v in per.items()}
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = P * args.steps / elapsed
+
+    nbytes = algorithmic_bytes(wl, ell, P)
+    dominant = max(("gc_encode", "gc_reconstruct"), key=lambda n: avg_ms[n])
+    achieved = nbytes[dominant] / (avg_ms[dominant] * 1e-3) / 1e9
+    gbs = {n: nbytes[n] / (avg_ms[n] * 1e-3) / 1e9 for n in names}
+
+    decs = dec.cpu().numpy()
+    se = sqerr.cpu().numpy()
+    out = {
+        "metric": METRIC, "value": value, "unit": "patterns/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "N": wl.N, "m": wl.m, "s": wl.s, "d": wl.d, "n": wl.n,
+                   "loss": wl.loss, "patterns": P, "ell": ell, "assignment": "cyclic",
+                   "stragglers": "10 full + uniform partial progress"},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes": nbytes[dominant], "avg_ms": avg_ms[dominant]},
+        "kernels_ms": avg_ms,
+        "kernels_gbs": gbs,
+        "decoded_gradients_per_s": float((decs == 1).sum()) * args.steps / elapsed,
+        "quality": {"decodable_frac": float((decs == 1).mean()),
+                    "mean_coef_err": float(cerr.float().mean().item()),
+                    "mse_vs_sum_g": float(se.mean() / wl.d),
+                    "mse_decodable": float(se[decs == 1].mean() / wl.d) if (decs == 1).any() else None},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, ell, X, y, w, psi, R, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -129,7 +129,7 @@ extern "C" int gc_chunk_grads(const float *X, const float *y, const float *W, in
   const bool vec4 = d % 4 == 0 && aligned16(X) && aligned16(W) && aligned16(G);
   const int vec = vec4 ? 4 : 1;
   const int64_t tiles = ceil_div(d, int64_t(kGradThreads) * vec);
-  if (ceil_div(rows, kGradWaves) > 0x7fffffffLL || int64_t(b) * N * tiles > 0x7fffffffLL)
+  if (!grid_ok(ceil_div(rows, kGradWaves), kGradThreads) || !grid_ok(int64_t(b) * N * tiles, kGradThreads))
     return GC_EINVAL;
   const int dev = check_device();
   if (dev != GC_OK) return dev;

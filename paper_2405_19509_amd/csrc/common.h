@@ -34,6 +34,11 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// A 1-D launch must keep gridDim.x < 2^31 and the total thread count < 2^32.
+inline bool grid_ok(int64_t blocks, int threads) {
+  return blocks >= 1 && blocks <= 0x7fffffffLL && blocks * threads <= 0xffffffffLL;
+}
+
 // bf16 bits -> fp32 (exact)
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);

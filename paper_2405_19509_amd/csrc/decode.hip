@@ -264,7 +264,7 @@ extern "C" int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_
       gamma < 1 || gamma > GC_MAX_DELTA || ell < 1 || ell > GC_MAX_ELL)
     return GC_EINVAL;
   if (P == 0) return GC_OK;
-  if (P > int64_t(kDecodeWaves) * 0x7fffffffLL) return GC_EINVAL;
+  if (!grid_ok(ceil_div(P, kDecodeWaves), kDecodeThreads)) return GC_EINVAL;
   if (!psi || !order || !holder || !hpos || !R || !cov || !dec || !coef_err || !Bc)
     return GC_EINVAL;
   const int dev = check_device();

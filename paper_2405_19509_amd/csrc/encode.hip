@@ -56,14 +56,21 @@ __device__ __forceinline__ void load_vec(const GT *p, float (&v)[VEC]) {
   for (int q = 0; q < VEC; ++q) v[q] = to_f32<GT>(e[q]);
 }
 
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+
+// T is written once and read back only by the combine: non-temporal stores
+// keep it from displacing the chunk-gradient slices in L2.
 template <int VEC>
 __device__ __forceinline__ void store_vec(float *p, const float (&v)[VEC]) {
   if constexpr (VEC == 4) {
-    *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    const v4f t = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(t, reinterpret_cast<v4f *>(p));
   } else if constexpr (VEC == 2) {
-    *reinterpret_cast<float2 *>(p) = make_float2(v[0], v[1]);
+    const v2f t = {v[0], v[1]};
+    __builtin_nontemporal_store(t, reinterpret_cast<v2f *>(p));
   } else {
-    *p = v[0];
+    __builtin_nontemporal_store(v[0], p);
   }
 }
 
@@ -193,7 +200,7 @@ int launch_encode(EncodeArgs a, hipStream_t st) {
   a.rows_per_block = kEncRowsPerBlock;
   const int64_t rblocks = ceil_div(a.rows, a.rows_per_block);
   const int64_t blocks = rblocks * a.nslices;
-  if (blocks > 0x7fffffffLL) return GC_EINVAL;
+  if (!grid_ok(blocks, kEncThreads)) return GC_EINVAL;
   const size_t lds = gbytes + per_row * group;
   if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_kernel<GT, VEC, STAGE>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)

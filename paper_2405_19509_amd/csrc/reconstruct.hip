@@ -3,95 +3,125 @@
 // target; and gc_sum_chunks, the exact target sum_i g_{D_i} itself.
 //
 // Bandwidth design (HBM-bound on the T read, ~0.5 flop per byte): a block
-// owns one pattern and one slice of 4096 consecutive x positions; each thread
-// keeps Q = 4096 / (256 * VEC) vectors of ell accumulators and, for every
-// worker j, issues its Q independent vector loads of T[p][j][slice] before
-// using any of them (Q loads in flight per thread, every T byte read once).
-// R[k][j] is a wave-uniform value read from LDS.  The squared error is
-// accumulated in fp64 per block and reduced across slices in a fixed order by
-// a second small kernel, so it is deterministic.
+// owns one pattern and one piece of 1024 consecutive x positions (4 KB of
+// every worker's row); consecutive blocks take consecutive pieces, so the
+// blocks in flight sweep each pattern's T rows as adjacent 4 KB pieces, the
+// read shape that measured fastest on MI355X.  Each thread holds one
+// float4 of ell accumulators and keeps UNR rows of loads in flight;
+// R[k][j] is a wave-uniform (scalar) load.  T is read with non-temporal
+// loads (it is consumed once).  The squared error is accumulated in fp64 per
+// block and reduced across pieces in a fixed order by a second small kernel,
+// so it is deterministic.
 #include "common.h"
 
 namespace gcx {
 namespace {
 
 constexpr int kRecThreads = 256;
-constexpr int64_t kRecSlice = 4096;
+constexpr int64_t kRecPiece = 1024;  // x positions per block
+constexpr int kRecUnroll = 4;        // rows of T loads in flight per thread
 
-size_t rec_slices(int64_t L) { return size_t(ceil_div(L, kRecSlice)); }
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+int64_t rec_pieces(int64_t L) { return ceil_div(L, kRecPiece); }
+
+// VEC = 4: thread t owns x = piece*1024 + 4t .. 4t+3 (needs L % 4 == 0 and aligned T);
+// VEC = 1: thread t owns x = piece*1024 + t + 256e, e < 4 (any L).
+template <int VEC>
+__device__ __forceinline__ int64_t rec_x(int64_t q, int e) {
+  return VEC == 4 ? q * kRecPiece + int64_t(threadIdx.x) * 4 + e
+                  : q * kRecPiece + threadIdx.x + int64_t(kRecThreads) * e;
+}
+
+template <int VEC>
+__device__ __forceinline__ void rec_load(const float *__restrict__ row, int64_t q, int64_t L, float (&v)[4]) {
+  if constexpr (VEC == 4) {
+    const int64_t x = rec_x<4>(q, 0);
+    if (x < L) {
+      const v4f t = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(row + x));
+      v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+    } else {
+      v[0] = v[1] = v[2] = v[3] = 0.f;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t x = rec_x<1>(q, e);
+      v[e] = x < L ? __builtin_nontemporal_load(row + x) : 0.f;
+    }
+  }
+}
 
 template <int ELL, int VEC>
 __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     const float *__restrict__ T, const float *__restrict__ R, int m, int64_t d, int64_t L,
-    int nslices, float *__restrict__ ghat, const float *__restrict__ gsum,
+    int64_t pieces, float *__restrict__ ghat, const float *__restrict__ gsum,
     double *__restrict__ partial) {
-  constexpr int Q = int(kRecSlice / (kRecThreads * VEC));
-  extern __shared__ float Rs[];  // [ELL][m]
   __shared__ double red[kRecThreads / kWave];
-  for (int a = threadIdx.x; a < ELL * m; a += kRecThreads) Rs[a] = R[a];
-  __syncthreads();
+  const int64_t p = blockIdx.x / pieces;
+  const int64_t q = blockIdx.x % pieces;
+  const float *Tp = T + p * int64_t(m) * L;
 
-  const int64_t p = blockIdx.x / nslices;
-  const int64_t s = blockIdx.x % nslices;
-  const int64_t xs = s * kRecSlice;
-
-  float acc[ELL][Q][VEC];
+  float acc[ELL][4];
 #pragma unroll
   for (int k = 0; k < ELL; ++k)
 #pragma unroll
-    for (int q = 0; q < Q; ++q)
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[k][q][e] = 0.f;
+    for (int e = 0; e < 4; ++e) acc[k][e] = 0.f;
 
-  const float *Tp = T + p * int64_t(m) * L;
-  for (int j = 0; j < m; ++j) {
-    float v[Q][VEC];
+  int j = 0;
+  for (; j + kRecUnroll <= m; j += kRecUnroll) {
+    float v[kRecUnroll][4];
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int64_t x = xs + (int64_t(q) * kRecThreads + threadIdx.x) * VEC;
-      if (x < L) {
-        const float *src = Tp + int64_t(j) * L + x;
-        if constexpr (VEC == 4) {
-          const float4 t4 = *reinterpret_cast<const float4 *>(src);
-          v[q][0] = t4.x; v[q][1] = t4.y; v[q][2] = t4.z; v[q][3] = t4.w;
-        } else {
+    for (int u = 0; u < kRecUnroll; ++u) rec_load<VEC>(Tp + int64_t(j + u) * L, q, L, v[u]);
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) v[q][e] = src[e];
-        }
-      } else {
+    for (int u = 0; u < kRecUnroll; ++u)
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) v[q][e] = 0.f;
+      for (int k = 0; k < ELL; ++k) {
+        const float r = R[int64_t(k) * m + j + u];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[k][e] = fmaf(r, v[u][e], acc[k][e]);
       }
-    }
+  }
+  for (; j < m; ++j) {
+    float v[4];
+    rec_load<VEC>(Tp + int64_t(j) * L, q, L, v);
 #pragma unroll
     for (int k = 0; k < ELL; ++k) {
-      const float r = Rs[k * m + j];
+      const float r = R[int64_t(k) * m + j];
 #pragma unroll
-      for (int q = 0; q < Q; ++q)
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[k][q][e] = fmaf(r, v[q][e], acc[k][q][e]);
+      for (int e = 0; e < 4; ++e) acc[k][e] = fmaf(r, v[e], acc[k][e]);
     }
   }
 
   double se = 0.0;
 #pragma unroll
-  for (int k = 0; k < ELL; ++k)
+  for (int k = 0; k < ELL; ++k) {
+    const int64_t x0 = rec_x<VEC>(q, 0);
+    const int64_t c0 = int64_t(k) * L + x0;
+    if (VEC == 4 && x0 < L && c0 + 3 < d) {  // whole float4 inside the gradient
+      if (ghat)
+        *reinterpret_cast<float4 *>(ghat + p * d + c0) = make_float4(acc[k][0], acc[k][1], acc[k][2], acc[k][3]);
+      if (partial) {
+        const float4 g = *reinterpret_cast<const float4 *>(gsum + c0);
+        const double e0 = double(acc[k][0]) - g.x, e1 = double(acc[k][1]) - g.y;
+        const double e2 = double(acc[k][2]) - g.z, e3 = double(acc[k][3]) - g.w;
+        se += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
+      }
+    } else {
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int64_t x = xs + (int64_t(q) * kRecThreads + threadIdx.x) * VEC;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const int64_t col = int64_t(k) * L + x + e;
-        if (x + e < L && col < d) {
-          const float gv = acc[k][q][e];
-          if (ghat) ghat[p * d + col] = gv;
+      for (int e = 0; e < 4; ++e) {
+        const int64_t x = rec_x<VEC>(q, e);
+        const int64_t col = int64_t(k) * L + x;
+        if (x < L && col < d) {
+          if (ghat) ghat[p * d + col] = acc[k][e];
           if (partial) {
-            const double diff = double(gv) - double(gsum[col]);
+            const double diff = double(acc[k][e]) - double(gsum[col]);
             se += diff * diff;
           }
         }
       }
     }
+  }
   if (partial) {
     se = wave_sum(se);
     if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = se;
@@ -99,7 +129,7 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     if (threadIdx.x == 0) {
       double tot = 0.0;
       for (int w = 0; w < kRecThreads / kWave; ++w) tot += red[w];
-      partial[p * nslices + s] = tot;
+      partial[p * pieces + q] = tot;
     }
   }
 }
@@ -115,15 +145,14 @@ __global__ void sqerr_finalize_kernel(const double *__restrict__ partial, int64_
 
 template <int ELL>
 void launch_rec(bool vec4, const float *T, const float *R, int64_t P, int m, int64_t d, int64_t L,
-                int nslices, float *ghat, const float *gsum, double *partial, hipStream_t st) {
-  const int64_t blocks = P * nslices;
-  const size_t lds = sizeof(float) * ELL * m;
+                int64_t pieces, float *ghat, const float *gsum, double *partial, hipStream_t st) {
+  const dim3 grid(unsigned(P * pieces));
   if (vec4)
-    hipLaunchKernelGGL((reconstruct_kernel<ELL, 4>), dim3(unsigned(blocks)), dim3(kRecThreads), lds,
-                       st, T, R, m, d, L, nslices, ghat, gsum, partial);
+    hipLaunchKernelGGL((reconstruct_kernel<ELL, 4>), grid, dim3(kRecThreads), 0, st, T, R, m, d, L,
+                       pieces, ghat, gsum, partial);
   else
-    hipLaunchKernelGGL((reconstruct_kernel<ELL, 1>), dim3(unsigned(blocks)), dim3(kRecThreads), lds,
-                       st, T, R, m, d, L, nslices, ghat, gsum, partial);
+    hipLaunchKernelGGL((reconstruct_kernel<ELL, 1>), grid, dim3(kRecThreads), 0, st, T, R, m, d, L,
+                       pieces, ghat, gsum, partial);
 }
 
 __global__ void sum_chunks_kernel(const void *__restrict__ G, int bf16, int N, int64_t d,
@@ -147,8 +176,8 @@ __global__ void sum_chunks_kernel(const void *__restrict__ G, int bf16, int N, i
 extern "C" size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell) {
   (void)m;
   if (P < 1 || d < 1 || ell < 1 || ell > GC_MAX_ELL) return 0;
-  const size_t ns = gcx::rec_slices(gcx::ceil_div(d, ell));
-  return ns > 1 ? sizeof(double) * size_t(P) * ns : 0;
+  const int64_t pieces = gcx::rec_pieces(gcx::ceil_div(d, ell));
+  return pieces > 1 ? sizeof(double) * size_t(P) * size_t(pieces) : 0;
 }
 
 extern "C" int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t m, int64_t d,
@@ -162,11 +191,11 @@ extern "C" int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t
   if (want_err && !gsum) return GC_EINVAL;
   if (!ghat && !want_err) return GC_OK;  // nothing requested
   const int64_t L = ceil_div(d, ell);
-  const int nslices = int(rec_slices(L));
-  if (P * nslices > 0x7fffffffLL) return GC_EINVAL;
+  const int64_t pieces = rec_pieces(L);
+  if (!grid_ok(P * pieces, kRecThreads)) return GC_EINVAL;
   double *partial = nullptr;
   if (want_err) {
-    if (nslices == 1) {
+    if (pieces == 1) {
       partial = sqerr;
     } else {
       const size_t need = gc_reconstruct_workspace_size(P, m, d, ell);
@@ -176,20 +205,22 @@ extern "C" int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t
   }
   const int dev = check_device();
   if (dev != GC_OK) return dev;
-  const bool vec4 = (L % 4 == 0) && aligned16(T);
+  // float4 path: rows of T, the estimate's rows and gsum all 16-byte aligned
+  const bool vec4 = L % 4 == 0 && d % 4 == 0 && aligned16(T) && (!ghat || aligned16(ghat)) &&
+                    (!gsum || aligned16(gsum));
   (void)hipGetLastError();
   switch (ell) {
 #define GC_CASE(E)                                                                           \
   case E:                                                                                    \
-    launch_rec<E>(vec4, T, R, P, m, d, L, nslices, ghat, gsum, partial, stream);             \
+    launch_rec<E>(vec4, T, R, P, m, d, L, pieces, ghat, gsum, partial, stream);              \
     break;
     GC_CASE(1) GC_CASE(2) GC_CASE(3) GC_CASE(4) GC_CASE(5) GC_CASE(6) GC_CASE(7) GC_CASE(8)
 #undef GC_CASE
     default: return GC_EINVAL;
   }
-  if (want_err && nslices > 1)
+  if (want_err && pieces > 1)
     hipLaunchKernelGGL(sqerr_finalize_kernel, dim3(unsigned(ceil_div(P, 256))), dim3(256), 0,
-                       stream, partial, P, nslices, sqerr);
+                       stream, partial, P, int(pieces), sqerr);
   return launch_status();
 }
 
@@ -197,7 +228,7 @@ extern "C" int gc_sum_chunks(const void *G, int32_t g_dtype, int32_t N, int64_t 
                              hipStream_t stream) {
   using namespace gcx;
   if (N < 1 || d < 1 || !G || !gsum || (g_dtype != GC_F32 && g_dtype != GC_BF16)) return GC_EINVAL;
-  if (ceil_div(d, 256) > 0x7fffffffLL) return GC_EINVAL;
+  if (!grid_ok(ceil_div(d, 256), 256)) return GC_EINVAL;
   const int dev = check_device();
   if (dev != GC_OK) return dev;
   (void)hipGetLastError();
