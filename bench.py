@@ -45,12 +45,14 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(wl, ell, P):
-    """Compulsory bytes per launch: every input read once, every output written once."""
+def algorithmic_bytes(wl, ell, P, sent):
+    """Compulsory bytes per launch: every input read once, every output written once.
+    ``sent`` = number of (pattern, worker) rows that transmit (psi > 0): only those
+    rows of T are written by the encode and read by the combine."""
     m, N, d, delta = wl.m, wl.N, wl.d, wl.delta
     L = -(-d // ell)
-    enc = 4 * P * m * L + 4 * N * d + 4 * P * m + 4 * P * m * delta * ell + 4 * m * delta
-    rec = 4 * P * m * L + 4 * P * d + 4 * ell * m + 4 * d + 8 * P
+    enc = 4 * sent * L + 4 * N * d + 4 * P * m + 4 * P * m * delta * ell + 4 * m * delta
+    rec = 4 * sent * L + 4 * P * m + 4 * P * d + 4 * ell * m + 4 * d + 8 * P
     dcd = 4 * P * m + 4 * P * N + P + 4 * P + 4 * P * m * delta * ell + 4 * ell * m + 12 * N * delta
     grads = 4 * N * wl.n * wl.d + 4 * N * wl.n + 4 * d + 4 * N * d
     return {"gc_encode": enc, "gc_reconstruct": rec, "gc_decode_coeffs": dcd, "gc_chunk_grads": grads,
@@ -151,7 +153,7 @@ def main():
         mark(3)
         gcx.gc_encode(G, psid, orderd, Bc, T=T)
         mark(4)
-        gcx.gc_reconstruct(T, Rd, wl.d, ghat=ghat, gsum=gsum, sqerr=sqerr, workspace=ws_r)
+        gcx.gc_reconstruct(T, Rd, wl.d, psi=psid, ghat=ghat, gsum=gsum, sqerr=sqerr, workspace=ws_r)
         mark(5)
 
     # a plain copy of known size, for calibrating HBM byte counters
@@ -184,7 +186,8 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
     value = P * args.steps / elapsed
 
-    nbytes = algorithmic_bytes(wl, ell, P)
+    sent = int((psi > 0).sum())
+    nbytes = algorithmic_bytes(wl, ell, P, sent)
     dominant = max(("gc_encode", "gc_reconstruct"), key=lambda n: avg_ms[n])
     achieved = nbytes[dominant] / (avg_ms[dominant] * 1e-3) / 1e9
     gbs = {n: nbytes[n] / (avg_ms[n] * 1e-3) / 1e9 for n in names}
@@ -197,7 +200,8 @@ def main():
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": wl.name, "N": wl.N, "m": wl.m, "s": wl.s, "d": wl.d, "n": wl.n,
                    "loss": wl.loss, "patterns": P, "ell": ell, "assignment": "cyclic",
-                   "stragglers": "10 full + uniform partial progress"},
+                   "stragglers": "10 full + uniform partial progress",
+                   "transmitting_rows_frac": sent / (P * wl.m)},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "algorithmic_bytes": nbytes[dominant], "avg_ms": avg_ms[dominant]},

@@ -158,8 +158,10 @@ int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m, const 
  * gc_encode -- what every worker transmits (Sec. 2, worker encode): for each
  * pattern p and worker j,
  *   T[p][j][x] = sum_{t < psi[p][j]} sum_{k < ell} Bc[p][j][t][k] * g_{order[j][t]}[k*L + x]
- * for 0 <= x < L, over the worker's processed prefix only (a worker with
- * psi = 0 sends zeros).  G [N][d] device in g_dtype; psi [P][m], order
+ * for 0 <= x < L, over the worker's processed prefix only.  A worker with
+ * psi[p][j] <= 0 has processed nothing and transmits nothing (a straggler in
+ * the sense of Sec. 1): its row T[p][j] is NOT written and keeps whatever it
+ * held.  G [N][d] device in g_dtype; psi [P][m], order
  * [m][delta] int32 device; Bc [P][m][delta][ell] fp32 device (as from
  * gc_decode_coeffs); T [P][m][L] fp32 device.  fp32 accumulation.  psi is
  * clamped to [0, delta] and padded order slots are skipped.
@@ -170,8 +172,10 @@ int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_
 
 /*
  * gc_reconstruct -- the PS combine (Sec. 2.2, last step): block k of the
- * estimate is sum_j R[k][j] T[p][j][:], i.e.
- *   ghat[p][k*L + x] = sum_j R[k][j] * T[p][j][x]   for k*L + x < d.
+ * estimate is sum_j R[k][j] T[p][j][:] over the workers that transmitted, i.e.
+ *   ghat[p][k*L + x] = sum_{j : psi[p][j] > 0} R[k][j] * T[p][j][x]   for k*L + x < d.
+ * psi [P][m] int32 device, or NULL to combine every row of T (then rows of
+ * non-transmitting workers must hold zeros).  Rows with psi <= 0 are not read.
  * Equals sum_i g_{D_i} when the pattern is decodable; otherwise it is the
  * least-squares estimate.  If gsum is non-NULL and sqerr non-NULL,
  *   sqerr[p] = sum_x (ghat[p][x] - gsum[x])^2   (fp64 accumulation)
@@ -182,9 +186,9 @@ int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_
  * deterministic).
  */
 size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell);
-int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t m, int64_t d, int32_t ell,
-                   float *ghat, const float *gsum, double *sqerr, void *workspace,
-                   size_t workspace_bytes, hipStream_t stream);
+int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
+                   int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -1,5 +1,7 @@
 // gc_encode: every simulated worker's transmitted vector (Sec. 2, worker encode)
 //   T[p][j][x] = sum_{t < psi[p][j]} sum_{k < ell} Bc[p][j][t][k] * g_{order[j][t]}[k*L + x]
+// Workers with psi = 0 transmit nothing (they are the stragglers of Sec. 1);
+// their rows of T are not written.
 //
 // Bandwidth design (HBM-bound on the T write, ~1 flop per byte):
 //   - a block owns one slice of W consecutive x positions and a contiguous
@@ -24,6 +26,7 @@ constexpr int kEncWaves = kEncThreads / kWave;
 constexpr size_t kEncSliceLds = 96 * 1024;   // G slice budget
 constexpr size_t kEncMetaLds = 24 * 1024;    // row metadata budget
 constexpr int64_t kEncRowsPerBlock = 4096;
+constexpr int kEncMaxGroup = 1024;           // rows of metadata staged per step, at most
 
 template <typename GT>
 __device__ __forceinline__ float to_f32(GT v);
@@ -136,15 +139,22 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int stride_row = a.delta * a.ell;
   const int64_t xl = x0 + int64_t(lane) * VEC;  // this lane's first x
+  __shared__ int nact;                          // rows of the group that transmit
+  __shared__ int16_t act[kEncMaxGroup];
   for (int64_t g0 = r0; g0 < r1; g0 += a.group_rows) {
     const int gn = int(r1 - g0 < a.group_rows ? r1 - g0 : a.group_rows);
     __syncthreads();  // previous group fully consumed (and the slice staged)
+    if (threadIdx.x == 0) nact = 0;
+    __syncthreads();
     for (int e = threadIdx.x; e < gn; e += kEncThreads) {
       const int64_t r = g0 + e;
       const int j = int(r % a.m);
       int v = a.psi[r];
       v = v < 0 ? 0 : (v > a.delta ? a.delta : v);
       mpsi[e] = v;
+      // a worker that has processed nothing transmits nothing: only the other
+      // rows are queued, so the waves share the transmitted rows evenly
+      if (v > 0) act[atomicAdd(&nact, 1)] = int16_t(e);
       for (int t = 0; t < a.delta; ++t) {
         int c = a.order[int64_t(j) * a.delta + t];
         mchunk[e * a.delta + t] = (c >= 0 && c < a.N) ? c : -1;
@@ -154,7 +164,9 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
     for (int e = threadIdx.x; e < gn * stride_row; e += kEncThreads) mcoef[e] = src[e];
     __syncthreads();
 
-    for (int e = wave; e < gn; e += kEncWaves) {
+    const int na = nact;
+    for (int ai = wave; ai < na; ai += kEncWaves) {
+      const int e = act[ai];
       const int64_t r = g0 + e;
       const int np = mpsi[e];
       float acc[VEC];
@@ -194,7 +206,7 @@ int launch_encode(EncodeArgs a, hipStream_t st) {
       STAGE ? (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15) : size_t(0);
   const size_t per_row = sizeof(int32_t) * (1 + a.delta) + sizeof(float) * a.delta * a.ell;
   int group = int(kEncMetaLds / per_row);
-  if (group > 1024) group = 1024;
+  if (group > kEncMaxGroup) group = kEncMaxGroup;
   if (group < 1) group = 1;
   a.group_rows = group;
   a.rows_per_block = kEncRowsPerBlock;

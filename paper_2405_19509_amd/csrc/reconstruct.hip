@@ -11,7 +11,8 @@
 // R[k][j] is a wave-uniform (scalar) load.  T is read with non-temporal
 // loads (it is consumed once).  The squared error is accumulated in fp64 per
 // block and reduced across pieces in a fixed order by a second small kernel,
-// so it is deterministic.
+// so it is deterministic.  Given psi, rows of workers with psi = 0 (which
+// transmitted nothing) are neither read nor needed.
 #include "common.h"
 
 namespace gcx {
@@ -54,13 +55,31 @@ __device__ __forceinline__ void rec_load(const float *__restrict__ row, int64_t 
 
 template <int ELL, int VEC>
 __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
-    const float *__restrict__ T, const float *__restrict__ R, int m, int64_t d, int64_t L,
-    int64_t pieces, float *__restrict__ ghat, const float *__restrict__ gsum,
-    double *__restrict__ partial) {
+    const float *__restrict__ T, const float *__restrict__ R, const int32_t *__restrict__ psi,
+    int m, int64_t d, int64_t L, int64_t pieces, float *__restrict__ ghat,
+    const float *__restrict__ gsum, double *__restrict__ partial) {
   __shared__ double red[kRecThreads / kWave];
+  __shared__ int16_t rows[GC_MAX_M];  // the workers that transmitted, ascending
+  __shared__ int nrows;
   const int64_t p = blockIdx.x / pieces;
   const int64_t q = blockIdx.x % pieces;
   const float *Tp = T + p * int64_t(m) * L;
+
+  // compact the transmitting workers (psi > 0) with ballots in wave 0; with
+  // no psi every worker counts as transmitting
+  if (threadIdx.x < kWave) {
+    int cnt = 0;
+    for (int base = 0; base < m; base += kWave) {
+      const int j = base + int(threadIdx.x);
+      const bool on = j < m && (psi == nullptr || psi[p * m + j] > 0);
+      const unsigned long long mask = __ballot(on);
+      if (on) rows[cnt + __popcll(mask & ((1ull << threadIdx.x) - 1))] = int16_t(j);
+      cnt += __popcll(mask);
+    }
+    if (threadIdx.x == 0) nrows = cnt;
+  }
+  __syncthreads();
+  const int nr = nrows;
 
   float acc[ELL][4];
 #pragma unroll
@@ -68,21 +87,26 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[k][e] = 0.f;
 
-  int j = 0;
-  for (; j + kRecUnroll <= m; j += kRecUnroll) {
+  int a = 0;
+  for (; a + kRecUnroll <= nr; a += kRecUnroll) {
+    int jj[kRecUnroll];
     float v[kRecUnroll][4];
 #pragma unroll
-    for (int u = 0; u < kRecUnroll; ++u) rec_load<VEC>(Tp + int64_t(j + u) * L, q, L, v[u]);
+    for (int u = 0; u < kRecUnroll; ++u) {
+      jj[u] = rows[a + u];
+      rec_load<VEC>(Tp + int64_t(jj[u]) * L, q, L, v[u]);
+    }
 #pragma unroll
     for (int u = 0; u < kRecUnroll; ++u)
 #pragma unroll
       for (int k = 0; k < ELL; ++k) {
-        const float r = R[int64_t(k) * m + j + u];
+        const float r = R[int64_t(k) * m + jj[u]];
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[k][e] = fmaf(r, v[u][e], acc[k][e]);
       }
   }
-  for (; j < m; ++j) {
+  for (; a < nr; ++a) {
+    const int j = rows[a];
     float v[4];
     rec_load<VEC>(Tp + int64_t(j) * L, q, L, v);
 #pragma unroll
@@ -144,15 +168,16 @@ __global__ void sqerr_finalize_kernel(const double *__restrict__ partial, int64_
 }
 
 template <int ELL>
-void launch_rec(bool vec4, const float *T, const float *R, int64_t P, int m, int64_t d, int64_t L,
-                int64_t pieces, float *ghat, const float *gsum, double *partial, hipStream_t st) {
+void launch_rec(bool vec4, const float *T, const float *R, const int32_t *psi, int64_t P, int m,
+                int64_t d, int64_t L, int64_t pieces, float *ghat, const float *gsum, double *partial,
+                hipStream_t st) {
   const dim3 grid(unsigned(P * pieces));
   if (vec4)
-    hipLaunchKernelGGL((reconstruct_kernel<ELL, 4>), grid, dim3(kRecThreads), 0, st, T, R, m, d, L,
-                       pieces, ghat, gsum, partial);
+    hipLaunchKernelGGL((reconstruct_kernel<ELL, 4>), grid, dim3(kRecThreads), 0, st, T, R, psi, m, d,
+                       L, pieces, ghat, gsum, partial);
   else
-    hipLaunchKernelGGL((reconstruct_kernel<ELL, 1>), grid, dim3(kRecThreads), 0, st, T, R, m, d, L,
-                       pieces, ghat, gsum, partial);
+    hipLaunchKernelGGL((reconstruct_kernel<ELL, 1>), grid, dim3(kRecThreads), 0, st, T, R, psi, m, d,
+                       L, pieces, ghat, gsum, partial);
 }
 
 __global__ void sum_chunks_kernel(const void *__restrict__ G, int bf16, int N, int64_t d,
@@ -180,8 +205,8 @@ extern "C" size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d,
   return pieces > 1 ? sizeof(double) * size_t(P) * size_t(pieces) : 0;
 }
 
-extern "C" int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t m, int64_t d,
-                              int32_t ell, float *ghat, const float *gsum, double *sqerr,
+extern "C" int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P,
+                              int32_t m, int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
                               void *workspace, size_t workspace_bytes, hipStream_t stream) {
   using namespace gcx;
   if (P < 0 || m < 1 || m > GC_MAX_M || d < 1 || ell < 1 || ell > GC_MAX_ELL) return GC_EINVAL;
@@ -212,7 +237,7 @@ extern "C" int gc_reconstruct(const float *T, const float *R, int64_t P, int32_t
   switch (ell) {
 #define GC_CASE(E)                                                                           \
   case E:                                                                                    \
-    launch_rec<E>(vec4, T, R, P, m, d, L, pieces, ghat, gsum, partial, stream);              \
+    launch_rec<E>(vec4, T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, stream);         \
     break;
     GC_CASE(1) GC_CASE(2) GC_CASE(3) GC_CASE(4) GC_CASE(5) GC_CASE(6) GC_CASE(7) GC_CASE(8)
 #undef GC_CASE

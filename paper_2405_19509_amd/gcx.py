@@ -41,7 +41,7 @@ SIGNATURES = {
                                     _p, _p, _p, _p, _p]),
     "gc_encode": (_c.c_int, [_p, _i32, _i32, _i64, _p, _p, _p, _i64, _i32, _i32, _i32, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
-    "gc_reconstruct": (_c.c_int, [_p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
+    "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
 }
 
 _lib = None
@@ -234,10 +234,10 @@ def gc_reconstruct_workspace_size(P: int, m: int, d: int, ell: int) -> int:
     return int(load().gc_reconstruct_workspace_size(P, m, d, ell))
 
 
-def gc_reconstruct(T, R, d: int, ghat=None, gsum=None, sqerr=None, want_ghat: bool = True,
+def gc_reconstruct(T, R, d: int, psi=None, ghat=None, gsum=None, sqerr=None, want_ghat: bool = True,
                    workspace=None, stream=None):
-    """T [P][m][L], R [ell][m] -> (ghat [P][d] or None, sqerr [P] fp64 or None).
-    sqerr is computed when gsum [d] is given."""
+    """T [P][m][L], R [ell][m], psi [P][m] (or None: combine every row) ->
+    (ghat [P][d] or None, sqerr [P] fp64 or None).  sqerr is computed when gsum [d] is given."""
     torch = _torch()
     P, m, L = T.shape
     ell = R.shape[0]
@@ -256,7 +256,8 @@ def gc_reconstruct(T, R, d: int, ghat=None, gsum=None, sqerr=None, want_ghat: bo
         if workspace is not None:
             ws_ptr, ws_bytes = _dev(workspace, "workspace", torch.uint8), workspace.numel()
     st = load().gc_reconstruct(
-        _dev(T, "T", torch.float32), _dev(R, "R", torch.float32, (ell, m)), P, m, d, ell,
+        _dev(T, "T", torch.float32), _dev(R, "R", torch.float32, (ell, m)),
+        _dev(psi, "psi", torch.int32, (P, m)) if psi is not None else None, P, m, d, ell,
         _dev(ghat, "ghat", torch.float32, (P, d)) if ghat is not None else None,
         _dev(gsum, "gsum", torch.float32, (d,)) if gsum is not None else None,
         _dev(sqerr, "sqerr", torch.float64, (P,)) if sqerr is not None else None,

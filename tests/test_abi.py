@@ -103,16 +103,21 @@ def test_device_calls_validate_on_the_host():
     assert lib.gc_encode(p, 0, 6, 0, p, p, p, 4, 6, 3, 1, p, None) == E                        # d = 0
     assert lib.gc_encode(None, 0, 6, 64, p, p, p, 4, 6, 3, 1, p, None) == E                    # null G
     assert lib.gc_encode(p, 0, 6, 64, p, p, p, 0, 6, 3, 1, p, None) == gcx.GC_OK                # P = 0
-    assert lib.gc_reconstruct(p, p, 4, 6, 64, 0, p, None, None, None, 0, None) == E            # ell = 0
-    assert lib.gc_reconstruct(p, p, 4, 6, 64, 1, p, None, p, None, 0, None) == E               # sqerr w/o gsum
-    assert lib.gc_reconstruct(p, p, 4, 6, 1 << 20, 1, None, p, p, None, 0, None) == E          # workspace
+    assert lib.gc_reconstruct(p, p, p, 4, 6, 64, 0, p, None, None, None, 0, None) == E         # ell = 0
+    assert lib.gc_reconstruct(p, p, p, 4, 6, 64, 1, p, None, p, None, 0, None) == E            # sqerr w/o gsum
+    assert lib.gc_reconstruct(p, p, None, 4, 6, 1 << 20, 1, None, p, p, None, 0, None) == E    # workspace
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 5, p, p, 1 << 20, None) == E                # loss
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 0, p, p, 4, None) == E                      # small ws
     assert lib.gc_sum_chunks(p, 3, 2, 8, p, None) == E
 
 
 def test_workspace_sizes():
-    assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 1) == 4 * 50 * 512
-    assert gcx.gc_reconstruct_workspace_size(10000, 50, 16384, 1) == 8 * 10000 * 4
-    assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 1) == 0
-    assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 32
+    # fused single-pass path (d % 4 == 0, d <= 16384): two d-float partial slots per block
+    assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 1) == 4 * 512 * 2 * 16384
+    # general path: one residual per sample row and point
+    assert gcx.gc_chunk_grads_workspace_size(50, 512, 16385, 2) == 4 * 2 * 50 * 512
+    # one fp64 partial per (pattern, 1024-wide piece of a block), none when a block has one piece
+    assert gcx.gc_reconstruct_workspace_size(10000, 50, 16384, 1) == 8 * 10000 * 16
+    assert gcx.gc_reconstruct_workspace_size(10, 50, 1024, 1) == 0
+    assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 4) == 0
+    assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 128

@@ -200,18 +200,27 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     G = _data_G(wl)
     Gw = OP.widen(G, wl.g_dtype)
     # encode on identical inputs: G, psi and the oracle's coefficients rounded to fp32
-    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32)))
+    # T starts as NaN: rows of workers that transmit nothing (psi = 0) must stay untouched
+    Td = torch.full((len(psi), wl.m, -(-wl.d // ell)), float("nan"), device="cuda")
+    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32), T=Td))
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, Gw, ell)
+    sent = psi > 0
+    assert np.isnan(T[~sent]).all()
     bound = R_.gamma(nterm)[:, :, None] * M
-    diff = np.abs(T.astype(np.float64) - T_ref)
-    assert (diff <= bound).all(), f"T off by {np.max(diff - bound)}"
-    assert (T[psi == 0] == 0).all()
+    diff = np.abs(T[sent].astype(np.float64) - T_ref[sent])
+    assert (diff <= bound[sent]).all(), f"T off by {np.max(diff - bound[sent])}"
     # combine on identical inputs: the oracle's T rounded to fp32
     T32 = T_ref.astype(np.float32)
     gsum_ref = Gw.sum(axis=0)
     gsum32 = gsum_ref.astype(np.float32)
-    ghat, sqerr = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, gsum=dev(gsum32))
+    # the rows of non-transmitting workers are poisoned: given psi, they must not be read
+    T32_poison = T32.copy()
+    T32_poison[~sent] = np.nan
+    ghat, sqerr = gcx.gc_reconstruct(dev(T32_poison), dev(R), wl.d, psi=dev(psi), gsum=dev(gsum32))
     ghat, sqerr = host(ghat), host(sqerr)
+    # without psi every row is combined; the oracle's zero rows then give the same estimate
+    ghat_all, _ = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, gsum=dev(gsum32))
+    assert np.array_equal(host(ghat_all), ghat)
     gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, wl.d)
     gb = R_.gamma(wl.m) * mag
     gdiff = np.abs(ghat.astype(np.float64) - gh_ref)
@@ -220,7 +229,8 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     E = np.sqrt((gb ** 2).sum(axis=1))
     assert (np.abs(sqerr - se_ref) <= 2 * np.sqrt(se_ref) * E + E * E + 1e-12 * se_ref).all()
     # error-only mode gives the same sqerr
-    _, sq2 = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, gsum=dev(gsum32), want_ghat=False)
+    _, sq2 = gcx.gc_reconstruct(dev(T32_poison), dev(R), wl.d, psi=dev(psi), gsum=dev(gsum32),
+                                want_ghat=False)
     assert (host(sq2) == sqerr).all()
 
 
@@ -281,7 +291,7 @@ def test_end_to_end(wl, ell, count):
     gsum = gcx.gc_sum_chunks(Gd)
     _, _, _, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
     T = gcx.gc_encode(Gd, dev(psi), dev(order), Bc)
-    ghat, sqerr = gcx.gc_reconstruct(T, dev(R), wl.d, gsum=gsum)
+    ghat, sqerr = gcx.gc_reconstruct(T, dev(R), wl.d, psi=dev(psi), gsum=gsum)
     ghat, sqerr = host(ghat).astype(np.float64), host(sqerr)
     gh_ref = R_.end_to_end(O, psi, R, G_ref)
     rel = np.linalg.norm(ghat - gh_ref, axis=1) / np.maximum(np.linalg.norm(gh_ref, axis=1), 1e-300)
