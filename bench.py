@@ -59,6 +59,30 @@ def algorithmic_bytes(wl, ell, P, sent):
             "gc_sum_chunks": 4 * N * d + 4 * d}
 
 
+def measured_traffic(wl, call):
+    """HBM bytes per launch of the call's main kernel from the committed counter summary
+    (profiles/hbm_traffic_<workload>.txt), or None when that kernel's sources have changed
+    since the counters were taken."""
+    import hashlib
+    prefix = {"gc_encode": "encode_kernel", "gc_reconstruct": "reconstruct_kernel"}[call]
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{wl.name}.txt")
+    if not os.path.exists(path):
+        return None
+    data = None
+    for line in open(path):
+        if line.startswith("JSON "):
+            data = json.loads(line[5:])
+    if data is None:
+        return None
+    for name, k in data["kernels"].items():
+        if name.startswith(prefix):
+            h = hashlib.sha256()
+            for src in k["sources"]:
+                h.update(open(os.path.join(ROOT, src), "rb").read())
+            return k["hbm_bytes"] if h.hexdigest()[:16] == k["sources_sha256_16"] else None
+    return None
+
+
 def cpu_baseline(wl, ell, X, y, w, psi, R, budget_s):
     """The oracle as it stands, timed on this host on a bounded sample of the same workload."""
     import oracle.assignment as OA
@@ -203,7 +227,8 @@ def main():
                    "stragglers": "10 full + uniform partial progress",
                    "transmitting_rows_frac": sent / (P * wl.m)},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(wl, dominant) if ell == 1 else None,
                      "algorithmic_bytes": nbytes[dominant], "avg_ms": avg_ms[dominant]},
         "kernels_ms": avg_ms,
         "kernels_gbs": gbs,

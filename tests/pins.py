@@ -431,10 +431,22 @@ def pin_compact_layout():
                 assert np.all(Bc[j, psi[j]:] == 0)
 
 
+def pin_widen_bf16():
+    """bf16 storage: the stored 16 bits are the top half of an IEEE fp32 word (1 sign,
+    8 exponent, 7 mantissa bits); widening is exact."""
+    bits = np.array([0x3F80, 0xC000, 0x3F00, 0x0000, 0x8000, 0x4049, 0x7F7F, 0x0001], dtype=np.uint16)
+    want = [1.0, -2.0, 0.5, 0.0, -0.0, 3.140625, 3.3895313892515355e38, 9.183549615799121e-41]
+    got = OP.widen(bits, "bf16")
+    assert got.dtype == np.float64 and list(got) == want
+    assert np.signbit(got[4])
+    f = np.array([1.5, -0.25], dtype=np.float32)
+    assert list(OP.widen(f, "f32")) == [1.5, -0.25]
+
+
 ALL_PINS = [
     pin_fig1a_ordering, pin_cyclic_invariants, pin_tables_roundtrip,
     pin_grad_at_zero, pin_grad_finite_difference, pin_grad_multi_point,
     pin_fig1a_motivation, pin_sec2_2_support, pin_sec2_2_closed_forms, pin_remark1_ell1,
     pin_ls_optimality, pin_coef_err_identity, pin_worker_agreement, pin_two_routes,
-    pin_exact_recovery, pin_ell1_masked_sum, pin_compact_layout,
+    pin_exact_recovery, pin_ell1_masked_sum, pin_compact_layout, pin_widen_bf16,
 ]

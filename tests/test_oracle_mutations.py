@@ -77,6 +77,13 @@ def m_compact_shifted(B, O, ell):
     return np.roll(Bc, 1, axis=1)
 
 
+def m_widen_low_half(G, dtype="f32"):
+    if dtype == "bf16":
+        bits = np.asarray(G, dtype=np.uint16).astype(np.uint32)
+        return bits.view(np.float32).astype(np.float64)
+    return np.asarray(G, dtype=np.float64)
+
+
 def m_grad_sign(Xi, yi, w, loss):
     Xi = np.asarray(Xi, dtype=np.float64)
     z = Xi @ np.asarray(w, dtype=np.float64)
@@ -110,6 +117,7 @@ MUTANTS = [
     (OP, "blocks", m_blocks_strided),
     (OA, "cyclic_O", m_cyclic_reversed),
     (OP, "compact", m_compact_shifted),
+    (OP, "widen", m_widen_low_half),
     (OG, "chunk_gradient", m_grad_sign),
     (OG, "chunk_gradient", m_grad_no_sigmoid),
     (OG, "chunk_gradient", m_grad_residual_misindexed),
