@@ -108,3 +108,20 @@ def end_to_end(O, psi, R, G, per_worker=False):
 
 def chunk_grads(X, y, W, loss):
     return OG.chunk_gradients(X, y, W, loss)
+
+
+def sampled_blocks(G, dtype, ell, xs):
+    """Columns of the chunk gradients that block positions xs (in [0, L)) touch, laid out so
+    that ``OP.blocks(Gsub, ell)`` has block k = entries k*L + xs of the zero-padded gradients.
+    Lets the oracle compute T[:, xs] and the estimate at k*L + xs one by one at any d."""
+    G = np.asarray(G)
+    N, d = G.shape
+    L = -(-d // ell)
+    S = len(xs)
+    Gsub = np.zeros((N, ell * S))
+    for k in range(ell):
+        for s_, x in enumerate(xs):
+            c = k * L + int(x)
+            if c < d:
+                Gsub[:, k * S + s_] = OP.widen(G[:, c], dtype)
+    return Gsub

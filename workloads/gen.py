@@ -114,12 +114,23 @@ def given_chunk(wl: Workload, i: int, seed: int = 0, cols=None) -> np.ndarray:
     return g
 
 
-def given_G(wl: Workload, seed: int = 0, chunks=None) -> np.ndarray:
+def given_G(wl: Workload, seed: int = 0, chunks=None, threads: int = 1) -> np.ndarray:
+    """Chunk gradients [len(chunks)][d] in storage type; chunks are independent streams,
+    so ``threads`` > 1 generates them concurrently with identical values."""
     idx = list(range(wl.N)) if chunks is None else list(chunks)
     dt = np.uint16 if wl.g_dtype == "bf16" else np.float32
     G = np.empty((len(idx), wl.d), dtype=dt)
-    for a, i in enumerate(idx):
-        G[a] = given_chunk(wl, i, seed)
+
+    def fill(a):
+        G[a] = given_chunk(wl, idx[a], seed)
+
+    if threads > 1:
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(threads) as ex:
+            list(ex.map(fill, range(len(idx))))
+    else:
+        for a in range(len(idx)):
+            fill(a)
     return G
 
 
