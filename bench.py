@@ -29,6 +29,7 @@ if ROOT not in sys.path:
 
 METRIC = "straggler patterns decoded/sec at m=50,d=16384; HBM GB/s and MFMA % of peak"
 HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
 def parse():
@@ -40,6 +41,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--mfma-points", type=int, default=256,
+                    help="also time the chunk gradients at this many evaluation points (matrix-core "
+                         "path; 0 = skip); reported under 'mfma', outside the step")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of a plain device copy run once before warm-up (counter calibration)")
     return ap.parse_args()
@@ -81,6 +85,32 @@ def measured_traffic(wl, call):
                 h.update(open(os.path.join(ROOT, src), "rb").read())
             return k["hbm_bytes"] if h.hexdigest()[:16] == k["sources_sha256_16"] else None
     return None
+
+
+def time_many_points(gcx, wl, Xd, yd, b, dev, reps=5):
+    """Chunk gradients of the same X at b evaluation points: two fp32 GEMMs per chunk on the
+    matrix cores, 4 N n d b flops.  Reported against the fp32 MFMA peak."""
+    import torch
+    from workloads import gen
+    W = torch.from_numpy(gen.eval_points(wl, b)).to(dev)
+    G = torch.empty((b, wl.N, wl.d), dtype=torch.float32, device=dev)
+    ws = torch.empty(gcx.gc_chunk_grads_workspace_size(wl.N, wl.n, wl.d, b), dtype=torch.uint8, device=dev)
+    gcx.gc_chunk_grads(Xd, yd, W, gcx.GC_LOSS_LOGISTIC, G=G, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        gcx.gc_chunk_grads(Xd, yd, W, gcx.GC_LOSS_LOGISTIC, G=G, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    flops = 4.0 * wl.N * wl.n * wl.d * b
+    tf = flops / (ms * 1e-3) / 1e12
+    del G, ws, W
+    torch.cuda.empty_cache()
+    return {"bound": "mfma", "points": b, "ms": ms, "achieved": tf, "peak": FP32_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": tf / FP32_MFMA_PEAK_TFLOPS, "dtype": "f32",
+            "note": "gc_chunk_grads with W [b][d]: Z = X W^T, residuals, G = U^T X per chunk"}
 
 
 def cpu_baseline(wl, ell, X, y, w, psi, R, budget_s):
@@ -238,6 +268,8 @@ def main():
                     "mse_vs_sum_g": float(se.mean() / wl.d),
                     "mse_decodable": float(se[decs == 1].mean() / wl.d) if (decs == 1).any() else None},
     }
+    if args.mfma_points > 0:
+        out["mfma"] = time_many_points(gcx, wl, Xd, yd, args.mfma_points, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, ell, X, y, w, psi, R, args.cpu_seconds)
     print(json.dumps(out))

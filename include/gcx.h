@@ -106,8 +106,9 @@ int gc_assign(int32_t kind, int32_t N, int32_t m, int32_t s, int32_t *O, int32_t
  *   G[q][i][:] = X_i^T r,  r = X_i w_q - y_i          (GC_LOSS_LINEAR)
  *                          r = sigmoid(X_i w_q) - y_i (GC_LOSS_LOGISTIC)
  * X [N][n][d], y [N][n], W [b][d], G [b][N][d]: device fp32.  fp32 arithmetic.
- * workspace: device, at least gc_chunk_grads_workspace_size(N, n, d, b) bytes
- * (may be NULL when that size is 0).
+ * With b >= 16 points (b % 4 == 0, d % 4 == 0) the two contractions run on the
+ * fp32 matrix cores; X, y, W, G and the workspace must then be 16-byte aligned.
+ * workspace: device, at least gc_chunk_grads_workspace_size(N, n, d, b) bytes.
  * Errors: GC_EINVAL for sizes < 1, a null pointer, an unknown loss, or a
  * workspace that is too small.
  */

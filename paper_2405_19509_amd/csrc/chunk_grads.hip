@@ -15,6 +15,9 @@
 // block) and reduce_partials_kernel sums, for every chunk, the partials of
 // the blocks that touched it, in block order: one read of X, deterministic.
 //
+// Many points (b >= 16, b % 4 == 0, d % 4 == 0): two fp32 MFMA GEMMs per chunk
+// (chunk_grads_mfma.hip).
+//
 // General path (any d): two streaming kernels
 //   residual_kernel  one wavefront per sample row: dot(x, w) reduced across
 //                    the wave, then the loss residual  -> workspace r [b][N][n]
@@ -25,6 +28,13 @@
 #include "common.h"
 
 namespace gcx {
+
+// multi-point path on the matrix cores (chunk_grads_mfma.hip)
+bool mfma_eligible(int64_t d, int b);
+size_t mfma_workspace_bytes(int N, int n, int64_t d, int b);
+int launch_mfma_grads(const float *X, const float *y, const float *W, int N, int n, int64_t d, int b,
+                      int loss, float *G, void *workspace, hipStream_t st);
+
 namespace {
 
 constexpr int kGradThreads = 256;
@@ -246,6 +256,7 @@ bool fused_ok(int64_t d) { return d % 4 == 0 && d <= int64_t(gcx::kFusedThreads)
 
 extern "C" size_t gc_chunk_grads_workspace_size(int32_t N, int32_t n, int64_t d, int32_t b) {
   if (N < 1 || n < 1 || d < 1 || b < 1) return 0;
+  if (gcx::mfma_eligible(d, b)) return gcx::mfma_workspace_bytes(N, n, d, b);
   if (fused_ok(d)) {
     const gcx::FusedPlan fp = gcx::fused_plan(N, n);
     return sizeof(float) * size_t(b) * size_t(fp.blocks) * 2 * size_t(d);
@@ -270,6 +281,12 @@ extern "C" int gc_chunk_grads(const float *X, const float *y, const float *W, in
   const int dev = check_device();
   if (dev != GC_OK) return dev;
   (void)hipGetLastError();
+  if (mfma_eligible(d, b)) {
+    if (!vec4 || !aligned16(y) || !aligned16(workspace)) return GC_EINVAL;
+    const int st = launch_mfma_grads(X, y, W, N, n, d, b, loss, G, workspace, stream);
+    if (st != GC_OK) return st;
+    return launch_status();
+  }
   if (vec4 && fused_ok(d) && aligned16(workspace)) {
     const FusedPlan fp = fused_plan(N, n);
     if (!grid_ok(fp.blocks * b, kFusedThreads)) return GC_EINVAL;

@@ -32,7 +32,7 @@ inline int launch_status() {
 
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // A 1-D launch must keep gridDim.x < 2^31 and the total thread count < 2^32.
 inline bool grid_ok(int64_t blocks, int threads) {

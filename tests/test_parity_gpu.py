@@ -267,6 +267,33 @@ def test_chunk_grads_multi_point_and_ragged():
     assert G.shape == (3, 5, 1001) and rel.max() <= 1e-5
 
 
+MFMA_CASES = [(TINY, 16), (SMALL, 64), (HEADLINE, 32)]
+
+
+@pytest.mark.parametrize("wl,b", MFMA_CASES, ids=[f"{w.name}-b{b}" for w, b in MFMA_CASES])
+def test_chunk_grads_many_points_mfma(wl, b):
+    """b >= 16 points: the two contractions run on the fp32 matrix cores."""
+    X, y, _ = gen.regression_data(wl)
+    W = gen.eval_points(wl, b)
+    G = host(gcx.gc_chunk_grads(dev(X), dev(y), dev(W), 0 if wl.loss == "linear" else 1))
+    G_ref = R_.chunk_grads(X, y, W, wl.loss)
+    rel = np.linalg.norm(G - G_ref, axis=-1) / np.linalg.norm(G_ref, axis=-1)
+    assert G.shape == (b, wl.N, wl.d) and rel.max() <= 1e-5, rel.max()
+
+
+def test_chunk_grads_mfma_ragged_tiles():
+    """Row, point and column counts that are not multiples of the 128 x 128 tiles."""
+    wl = Workload(name="ragged_mfma", N=3, m=3, s=1, d=1000, P=1, ells=(1,), n=37, loss="logistic",
+                  x_std=0.05, w_std=0.1)
+    X, y, _ = gen.regression_data(wl)
+    for b in (20, 132):
+        W = gen.eval_points(wl, b)
+        G = host(gcx.gc_chunk_grads(dev(X), dev(y), dev(W), gcx.GC_LOSS_LOGISTIC))
+        G_ref = R_.chunk_grads(X, y, W, "logistic")
+        rel = np.linalg.norm(G - G_ref, axis=-1) / np.linalg.norm(G_ref, axis=-1)
+        assert rel.max() <= 1e-5, (b, rel.max())
+
+
 # ---------------------------------------------------------------------------
 # end to end: GPU pipeline vs full oracle
 # ---------------------------------------------------------------------------
