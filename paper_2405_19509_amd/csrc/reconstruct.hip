@@ -59,21 +59,27 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     int m, int64_t d, int64_t L, int64_t pieces, float *__restrict__ ghat,
     const float *__restrict__ gsum, double *__restrict__ partial) {
   __shared__ double red[kRecThreads / kWave];
-  __shared__ int16_t rows[GC_MAX_M];  // the workers that transmitted, ascending
+  __shared__ int rows[GC_MAX_M];      // the workers that transmitted, ascending
+  __shared__ float rw[ELL][GC_MAX_M];  // their R[k][j]
   __shared__ int nrows;
   const int64_t p = blockIdx.x / pieces;
   const int64_t q = blockIdx.x % pieces;
   const float *Tp = T + p * int64_t(m) * L;
 
-  // compact the transmitting workers (psi > 0) with ballots in wave 0; with
-  // no psi every worker counts as transmitting
+  // compact the transmitting workers (psi > 0) with ballots in wave 0, with their
+  // weights R[k][j]; with no psi every worker counts as transmitting
   if (threadIdx.x < kWave) {
     int cnt = 0;
     for (int base = 0; base < m; base += kWave) {
       const int j = base + int(threadIdx.x);
       const bool on = j < m && (psi == nullptr || psi[p * m + j] > 0);
       const unsigned long long mask = __ballot(on);
-      if (on) rows[cnt + __popcll(mask & ((1ull << threadIdx.x) - 1))] = int16_t(j);
+      if (on) {
+        const int a = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
+        rows[a] = j;
+#pragma unroll
+        for (int k = 0; k < ELL; ++k) rw[k][a] = R[int64_t(k) * m + j];
+      }
       cnt += __popcll(mask);
     }
     if (threadIdx.x == 0) nrows = cnt;
@@ -87,34 +93,32 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[k][e] = 0.f;
 
-  int a = 0;
-  for (; a + kRecUnroll <= nr; a += kRecUnroll) {
-    int jj[kRecUnroll];
-    float v[kRecUnroll][4];
-#pragma unroll
-    for (int u = 0; u < kRecUnroll; ++u) {
-      jj[u] = rows[a + u];
-      rec_load<VEC>(Tp + int64_t(jj[u]) * L, q, L, v[u]);
-    }
+  // software pipeline: the loads of the next kRecUnroll rows are in flight while the
+  // current ones are consumed
+  float va[kRecUnroll][4], vb[kRecUnroll][4];
+  auto issue = [&](int a0, float (&v)[kRecUnroll][4]) {
 #pragma unroll
     for (int u = 0; u < kRecUnroll; ++u)
+      if (a0 + u < nr) rec_load<VEC>(Tp + int64_t(rows[a0 + u]) * L, q, L, v[u]);
+  };
+  auto consume = [&](int a0, const float (&v)[kRecUnroll][4]) {
+#pragma unroll
+    for (int u = 0; u < kRecUnroll; ++u)
+      if (a0 + u < nr)
 #pragma unroll
       for (int k = 0; k < ELL; ++k) {
-        const float r = R[int64_t(k) * m + jj[u]];
+        const float r = rw[k][a0 + u];
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[k][e] = fmaf(r, v[u][e], acc[k][e]);
       }
-  }
-  for (; a < nr; ++a) {
-    const int j = rows[a];
-    float v[4];
-    rec_load<VEC>(Tp + int64_t(j) * L, q, L, v);
-#pragma unroll
-    for (int k = 0; k < ELL; ++k) {
-      const float r = R[int64_t(k) * m + j];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[k][e] = fmaf(r, v[e], acc[k][e]);
-    }
+  };
+  if (nr > 0) issue(0, va);
+  for (int a = 0; a < nr; a += 2 * kRecUnroll) {
+    if (a + kRecUnroll < nr) issue(a + kRecUnroll, vb);
+    consume(a, va);
+    if (a + kRecUnroll >= nr) break;
+    if (a + 2 * kRecUnroll < nr) issue(a + 2 * kRecUnroll, va);
+    consume(a + kRecUnroll, vb);
   }
 
   double se = 0.0;
