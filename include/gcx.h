@@ -52,6 +52,7 @@ extern "C" {
 /* assignment kinds for gc_assign */
 #define GC_ASSIGN_CYCLIC 0 /* cyclic scheme, N = m, worker j holds j..j+s (mod N) */
 #define GC_ASSIGN_ORDER 1  /* tables derived from a caller-given ordering matrix O */
+#define GC_ASSIGN_REGULAR 2 /* optimal ordering of a delta-regular support (Algorithm 2) */
 
 /* losses for gc_chunk_grads */
 #define GC_LOSS_LINEAR 0   /* l = (x.w - y)^2 / 2           */
@@ -89,6 +90,13 @@ const char *gc_strerror(int status);
  * kind = GC_ASSIGN_ORDER: O is an input; every column's non-zero entries must
  *   be 1..delta_j, once each (Sec. 3).  s is ignored.  delta >= max_j delta_j
  *   and gamma >= max_i gamma_i.
+ * kind = GC_ASSIGN_REGULAR: O is in/out.  On input its non-zero pattern is the
+ *   support of A, which must have N == m and exactly delta non-zeros in every
+ *   row and column (e.g. the adjacency matrix of a delta-regular graph); gamma
+ *   must equal delta.  Algorithm 2 (Chunk-Ordering, Sec. 3) peels delta perfect
+ *   matchings P_1..P_delta off the support (Hopcroft-Karp) and O is
+ *   overwritten with sum_i i * P_i, an ordering whose every row sums to
+ *   delta(delta+1)/2, the optimum of Q_max.  Orderings are not unique.
  *
  * Outputs (host, int32, -1 padded past a row's length):
  *   order  [m][delta]  chunk at position t of worker j
@@ -149,6 +157,8 @@ int gc_sum_chunks(const void *G, int32_t g_dtype, int32_t N, int64_t d, float *g
  * Requires 1 <= m <= GC_MAX_M, 1 <= delta, gamma <= GC_MAX_DELTA.
  * P = 0 is a no-op.  Invalid psi values are reported in dec, not by the return
  * value (psi is device data and is not read on the host).
+ * Coverage-only mode: Bc = NULL skips the solves (R may then be NULL too);
+ * cov may be NULL when only dec and coef_err are wanted.
  */
 int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m, const int32_t *order,
                      int32_t delta, const int32_t *holder, const int32_t *hpos, int32_t gamma,
@@ -186,6 +196,36 @@ int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_
  * (it holds per-slice partial sums, reduced in a fixed order, so sqerr is
  * deterministic).
  */
+/*
+ * gc_progress -- the straggler simulation of Sec. 4 at a grid of deadlines:
+ * worker j finishes the chunk at position t of its order at time
+ * sum_{u <= t} tau[r][j][u] (fp64, summed in position order); failed workers
+ * finish nothing.  psi[r][g][j] = number of chunks worker j has finished by T[g],
+ * i.e. the state vector the PS would broadcast at that deadline.
+ * tau [R][m][delta] fp64, failed [R][m] uint8 (non-zero = failed) or NULL,
+ * T [G] fp64, psi [R][G][m] int32: all device.
+ */
+int gc_progress(const double *tau, const uint8_t *failed, int64_t R, int32_t m, int32_t delta,
+                const double *T, int32_t G, int32_t *psi, hipStream_t stream);
+
+/*
+ * gc_completion_times -- exact-GC completion time of each trial (Sec. 4, the
+ * exact-GC simulation): the first time at which every chunk has been processed
+ * at least ell times, i.e. for each chunk the ell-th smallest finish time over
+ * its holders, maximised over chunks.
+ *   partial[r]   every processed chunk counts (the proposed protocol)
+ *   original[r]  only workers that have finished all delta of their chunks
+ *                count (original GC)
+ * +inf where failures leave some chunk with fewer than ell live holders.
+ * Every worker must hold delta chunks (tau [R][m][delta]).  tau fp64,
+ * failed [R][m] uint8 or NULL, holder/hpos [N][gamma] int32 (gc_assign),
+ * partial/original [R] fp64: all device.
+ */
+int gc_completion_times(const double *tau, const uint8_t *failed, int64_t R, int32_t N,
+                        int32_t m, int32_t delta, const int32_t *holder, const int32_t *hpos,
+                        int32_t gamma, int32_t ell, double *partial, double *original,
+                        hipStream_t stream);
+
 size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell);
 int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
                    int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,

@@ -12,5 +12,7 @@ Modules:
     gradients   per-chunk gradients g_{D_i} (Sec. 1)
     protocol    processed sets, coverage, decodability, Algorithm 1, encode,
                 PS combine (Sec. 2, Sec. 2.1, Sec. 2.2)
+    ordering    Algorithm 2, chunk ordering of regular assignments (Sec. 3)
+    simulation  worker progress and exact-GC completion times (Sec. 4)
 """
-from . import assignment, gradients, protocol  # noqa: F401
+from . import assignment, gradients, ordering, protocol, simulation  # noqa: F401

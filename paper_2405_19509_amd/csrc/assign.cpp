@@ -6,6 +6,7 @@
 // order (worker -> chunk by position), holder and hpos (chunk -> worker and
 // the position of the chunk inside that worker).
 #include <cstdint>
+#include <queue>
 #include <vector>
 
 #include "gcx.h"
@@ -59,6 +60,106 @@ int tables_from_order(int32_t N, int32_t m, const int32_t *O, int32_t delta, int
   return GC_OK;
 }
 
+// Maximum bipartite matching by Hopcroft-Karp: chunks on the left, workers on the
+// right, adj[i] the workers still available to chunk i.  Returns the matching size
+// and fills match_l (chunk -> worker) and match_r (worker -> chunk).
+int hopcroft_karp(const std::vector<std::vector<int32_t>> &adj, int32_t m,
+                  std::vector<int32_t> &match_l, std::vector<int32_t> &match_r) {
+  const int32_t N = int32_t(adj.size());
+  const int32_t INF = 1 << 30;
+  match_l.assign(N, -1);
+  match_r.assign(m, -1);
+  std::vector<int32_t> dist(N), it(N), stack;
+  int size = 0;
+  for (;;) {
+    // BFS layers from the free chunks
+    std::queue<int32_t> q;
+    for (int32_t i = 0; i < N; ++i) {
+      dist[i] = match_l[i] < 0 ? 0 : INF;
+      if (match_l[i] < 0) q.push(i);
+    }
+    bool found = false;
+    while (!q.empty()) {
+      const int32_t i = q.front();
+      q.pop();
+      for (int32_t j : adj[i]) {
+        const int32_t k = match_r[j];
+        if (k < 0) {
+          found = true;
+        } else if (dist[k] == INF) {
+          dist[k] = dist[i] + 1;
+          q.push(k);
+        }
+      }
+    }
+    if (!found) break;
+    // vertex-disjoint shortest augmenting paths, iterative DFS
+    for (int32_t i = 0; i < N; ++i) it[i] = 0;
+    for (int32_t root = 0; root < N; ++root) {
+      if (match_l[root] >= 0) continue;
+      stack.assign(1, root);
+      while (!stack.empty()) {
+        const int32_t i = stack.back();
+        if (it[i] >= int32_t(adj[i].size())) {
+          dist[i] = INF;  // dead end
+          stack.pop_back();
+          continue;
+        }
+        const int32_t j = adj[i][it[i]++];
+        const int32_t k = match_r[j];
+        if (k < 0) {
+          // augment along the stack: each chunk on it takes the worker it last tried
+          for (int32_t a = int32_t(stack.size()) - 1; a >= 0; --a) {
+            const int32_t u = stack[a];
+            const int32_t w = adj[u][it[u] - 1];
+            match_l[u] = w;
+            match_r[w] = u;
+          }
+          ++size;
+          stack.clear();
+        } else if (dist[k] == dist[i] + 1) {
+          stack.push_back(k);
+        }
+      }
+    }
+  }
+  return size;
+}
+
+// Algorithm 2 (Chunk-Ordering, Sec. 3): peel delta perfect matchings P_1..P_delta
+// off a delta-regular support and set O = sum_i i P_i.  Claim 1 guarantees each
+// perfect matching exists.  O is overwritten with the ordering.
+int regular_ordering(int32_t N, int32_t m, int32_t delta, int32_t *O) {
+  if (N != m) return GC_EINVAL;
+  std::vector<std::vector<int32_t>> adj(N);
+  std::vector<int32_t> coldeg(m, 0);
+  for (int32_t i = 0; i < N; ++i) {
+    for (int32_t j = 0; j < m; ++j)
+      if (O[int64_t(i) * m + j] != 0) {
+        adj[i].push_back(j);
+        ++coldeg[j];
+      }
+    if (int32_t(adj[i].size()) != delta) return GC_EINVAL;
+  }
+  for (int32_t j = 0; j < m; ++j)
+    if (coldeg[j] != delta) return GC_EINVAL;
+  std::vector<int32_t> out(size_t(N) * m, 0), ml, mr;
+  for (int32_t step = 1; step <= delta; ++step) {
+    if (hopcroft_karp(adj, m, ml, mr) != N) return GC_EINVAL;  // cannot happen for a regular support
+    for (int32_t i = 0; i < N; ++i) {
+      out[size_t(i) * m + ml[i]] = step;
+      auto &a = adj[i];
+      for (size_t u = 0; u < a.size(); ++u)
+        if (a[u] == ml[i]) {
+          a.erase(a.begin() + long(u));
+          break;
+        }
+    }
+  }
+  for (size_t a = 0; a < out.size(); ++a) O[a] = out[a];
+  return GC_OK;
+}
+
 }  // namespace
 
 extern "C" int gc_assign(int32_t kind, int32_t N, int32_t m, int32_t s, int32_t *O, int32_t delta,
@@ -78,6 +179,16 @@ extern "C" int gc_assign(int32_t kind, int32_t N, int32_t m, int32_t s, int32_t 
   if (kind == GC_ASSIGN_ORDER) {
     if (!O) return GC_EINVAL;
     return tables_from_order(N, m, O, delta, gamma, order, holder, hpos);
+  }
+  if (kind == GC_ASSIGN_REGULAR) {
+    if (!O || delta != gamma) return GC_EINVAL;
+    std::vector<int32_t> work(O, O + size_t(N) * m);
+    const int st = regular_ordering(N, m, delta, work.data());
+    if (st != GC_OK) return st;
+    const int st2 = tables_from_order(N, m, work.data(), delta, gamma, order, holder, hpos);
+    if (st2 == GC_OK)
+      for (size_t a = 0; a < work.size(); ++a) O[a] = work[a];
+    return st2;
   }
   return GC_EINVAL;
 }

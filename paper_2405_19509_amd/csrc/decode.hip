@@ -69,7 +69,8 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
     const float *__restrict__ R, int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
     int32_t *__restrict__ coef_err, float *__restrict__ Bc) {
   extern __shared__ float Rs[];  // [ELL][m]
-  for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
+  if (R != nullptr)
+    for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
   __syncthreads();  // the only barrier; every thread reaches it
 
   const int lane = threadIdx.x % kWave;
@@ -78,7 +79,8 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
 
   const int32_t *ps = psi + p * m;
   const int64_t wstride = int64_t(delta) * ELL;       // floats per worker in Bc
-  float *Bp = Bc + p * int64_t(m) * wstride;
+  const bool want_bc = Bc != nullptr;                  // else coverage only
+  float *Bp = want_bc ? Bc + p * int64_t(m) * wstride : nullptr;
 
   // psi_j must lie in [0, delta_j]; padded order slots get zero coefficients.
   bool bad = false;
@@ -88,7 +90,7 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
       const int c = order[int64_t(j) * delta + t];
       if (c >= 0 && c < N) {
         ++load;
-      } else {
+      } else if (want_bc) {
 #pragma unroll
         for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
       }
@@ -109,9 +111,10 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
       const int j = hi[u], t = hp[u];
       if (j >= 0 && j < m && t >= 0 && t < delta && ps[j] > t) ++Delta;
     }
-    cov[p * N + i] = Delta;
+    if (cov != nullptr) cov[p * N + i] = Delta;
     err += Delta < ELL ? ELL - Delta : 0;
     all_ok = all_ok && Delta >= ELL;
+    if (!want_bc) continue;
 
     if (Delta == 0 || invalid) {
       for (int u = 0; u < gamma; ++u) {
@@ -265,8 +268,8 @@ extern "C" int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_
     return GC_EINVAL;
   if (P == 0) return GC_OK;
   if (!grid_ok(ceil_div(P, kDecodeWaves), kDecodeThreads)) return GC_EINVAL;
-  if (!psi || !order || !holder || !hpos || !R || !cov || !dec || !coef_err || !Bc)
-    return GC_EINVAL;
+  if (!psi || !order || !holder || !hpos || !dec || !coef_err) return GC_EINVAL;
+  if (Bc && !R) return GC_EINVAL;
   const int dev = check_device();
   if (dev != GC_OK) return dev;
   (void)hipGetLastError();

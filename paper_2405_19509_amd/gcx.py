@@ -16,7 +16,7 @@ from typing import Optional
 import numpy as np
 
 GC_OK, GC_EINVAL, GC_ELAUNCH, GC_ENOTSUP = 0, -1, -2, -3
-GC_ASSIGN_CYCLIC, GC_ASSIGN_ORDER = 0, 1
+GC_ASSIGN_CYCLIC, GC_ASSIGN_ORDER, GC_ASSIGN_REGULAR = 0, 1, 2
 GC_LOSS_LINEAR, GC_LOSS_LOGISTIC = 0, 1
 GC_F32, GC_BF16 = 0, 1
 GC_DEC_NO, GC_DEC_YES, GC_DEC_INVALID = 0, 1, 2
@@ -40,6 +40,8 @@ SIGNATURES = {
     "gc_decode_coeffs": (_c.c_int, [_p, _i64, _i32, _i32, _p, _i32, _p, _p, _i32, _p, _i32,
                                     _p, _p, _p, _p, _p]),
     "gc_encode": (_c.c_int, [_p, _i32, _i32, _i64, _p, _p, _p, _i64, _i32, _i32, _i32, _p, _p]),
+    "gc_progress": (_c.c_int, [_p, _p, _i64, _i32, _i32, _p, _i32, _p, _p]),
+    "gc_completion_times": (_c.c_int, [_p, _p, _i64, _i32, _i32, _i32, _p, _p, _i32, _i32, _p, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
 }
@@ -121,7 +123,8 @@ def _g_dtype(G):
 
 def gc_assign(kind: int, N: int, m: int, s: int = -1, O: Optional[np.ndarray] = None,
               delta: Optional[int] = None, gamma: Optional[int] = None):
-    """Host call.  Returns (O, order, holder, hpos) as int32 numpy arrays."""
+    """Host call.  Returns (O, order, holder, hpos) as int32 numpy arrays.  For
+    GC_ASSIGN_REGULAR, O is the support on input and the returned O the ordering."""
     lib = load()
     if kind == GC_ASSIGN_CYCLIC:
         delta = s + 1 if delta is None else delta
@@ -183,9 +186,10 @@ def gc_sum_chunks(G, gsum=None, stream=None):
 
 
 def gc_decode_coeffs(psi, order, holder, hpos, R, cov=None, dec=None, coef_err=None, Bc=None,
-                     stream=None):
+                     coverage_only: bool = False, stream=None):
     """psi [P][m] int32, tables from gc_assign (device int32), R [ell][m] fp32
-    -> (cov [P][N] int32, dec [P] uint8, coef_err [P] int32, Bc [P][m][delta][ell] fp32)."""
+    -> (cov [P][N] int32, dec [P] uint8, coef_err [P] int32, Bc [P][m][delta][ell] fp32).
+    coverage_only: skip the coefficient solves (Bc is returned as None)."""
     torch = _torch()
     P, m = psi.shape
     m2, delta = order.shape
@@ -200,14 +204,14 @@ def gc_decode_coeffs(psi, order, holder, hpos, R, cov=None, dec=None, coef_err=N
         dec = torch.empty(P, dtype=torch.uint8, device=dv)
     if coef_err is None:
         coef_err = torch.empty(P, dtype=torch.int32, device=dv)
-    if Bc is None:
+    if Bc is None and not coverage_only:
         Bc = torch.empty((P, m, delta, ell), dtype=torch.float32, device=dv)
     st = load().gc_decode_coeffs(
         _dev(psi, "psi", torch.int32), P, N, m, _dev(order, "order", torch.int32), delta,
         _dev(holder, "holder", torch.int32), _dev(hpos, "hpos", torch.int32, (N, gamma)), gamma,
         _dev(R, "R", torch.float32), ell, _dev(cov, "cov", torch.int32, (P, N)),
         _dev(dec, "dec", torch.uint8, (P,)), _dev(coef_err, "coef_err", torch.int32, (P,)),
-        _dev(Bc, "Bc", torch.float32, (P, m, delta, ell)), _stream(stream))
+        _dev(Bc, "Bc", torch.float32, (P, m, delta, ell)) if Bc is not None else None, _stream(stream))
     _check("gc_decode_coeffs", st)
     return cov, dec, coef_err, Bc
 
@@ -264,3 +268,38 @@ def gc_reconstruct(T, R, d: int, psi=None, ghat=None, gsum=None, sqerr=None, wan
         ws_ptr, ws_bytes, _stream(stream))
     _check("gc_reconstruct", st)
     return ghat, sqerr
+
+
+def gc_progress(tau, T, failed=None, psi=None, stream=None):
+    """tau [R][m][delta] fp64, T [G] fp64, failed [R][m] uint8 or None -> psi [R][G][m] int32."""
+    torch = _torch()
+    R, m, delta = tau.shape
+    G = T.shape[0]
+    if psi is None:
+        psi = torch.empty((R, G, m), dtype=torch.int32, device=tau.device)
+    st = load().gc_progress(_dev(tau, "tau", torch.float64),
+                            _dev(failed, "failed", torch.uint8, (R, m)) if failed is not None else None,
+                            R, m, delta, _dev(T, "T", torch.float64, (G,)), G,
+                            _dev(psi, "psi", torch.int32, (R, G, m)), _stream(stream))
+    _check("gc_progress", st)
+    return psi
+
+
+def gc_completion_times(tau, holder, hpos, ell: int, failed=None, partial=None, original=None,
+                        stream=None):
+    """tau [R][m][delta] fp64, tables from gc_assign -> (partial [R], original [R]) fp64."""
+    torch = _torch()
+    R, m, delta = tau.shape
+    N, gamma = holder.shape
+    if partial is None:
+        partial = torch.empty(R, dtype=torch.float64, device=tau.device)
+    if original is None:
+        original = torch.empty(R, dtype=torch.float64, device=tau.device)
+    st = load().gc_completion_times(
+        _dev(tau, "tau", torch.float64),
+        _dev(failed, "failed", torch.uint8, (R, m)) if failed is not None else None, R, N, m, delta,
+        _dev(holder, "holder", torch.int32), _dev(hpos, "hpos", torch.int32, (N, gamma)), gamma, ell,
+        _dev(partial, "partial", torch.float64, (R,)), _dev(original, "original", torch.float64, (R,)),
+        _stream(stream))
+    _check("gc_completion_times", st)
+    return partial, original

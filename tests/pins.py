@@ -16,7 +16,9 @@ import numpy as np
 
 import oracle.assignment as OA
 import oracle.gradients as OG
+import oracle.ordering as OO
 import oracle.protocol as OP
+import oracle.simulation as OS
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
@@ -443,10 +445,131 @@ def pin_widen_bf16():
     assert list(OP.widen(f, "f32")) == [1.5, -0.25]
 
 
+# ---------------------------------------------------------------------------
+# Algorithm 2 (chunk ordering)
+# ---------------------------------------------------------------------------
+
+def _random_regular_support(g, m, delta):
+    """Union of delta disjoint random permutation matrices (a delta-regular bipartite support)."""
+    while True:
+        S = np.zeros((m, m), dtype=bool)
+        ok = True
+        for _ in range(delta):
+            for _try in range(200):
+                perm = g.permutation(m)
+                if not S[np.arange(m), perm].any():
+                    S[np.arange(m), perm] = True
+                    break
+            else:
+                ok = False
+                break
+        if ok:
+            return S
+
+
+def check_ordering(O, S):
+    """O is an ordering of support S whose every row sums to delta(delta+1)/2 (Sec. 3 optimum)."""
+    O = np.asarray(O)
+    delta = int(S.sum(axis=0)[0])
+    assert ((O != 0) == S).all()
+    for j in range(O.shape[1]):
+        assert sorted(O[S[:, j], j].tolist()) == list(range(1, delta + 1))
+    assert (O.sum(axis=1) == delta * (delta + 1) // 2).all()
+    assert OO.q_max(O) == delta * (delta + 1) // 2 + (O.shape[1] - delta - 1) * delta
+
+
+def pin_ordering_bruteforce_optimum():
+    """On tiny regular supports, Algorithm 2 reaches the minimum Q_max over every ordering
+    (each column's delta! orders enumerated)."""
+    g = rng(30)
+    for m, delta in [(4, 2), (5, 2), (4, 3), (5, 3)]:
+        S = _random_regular_support(g, m, delta)
+        per_col = []
+        for j in range(m):
+            rows = np.flatnonzero(S[:, j])
+            per_col.append([dict(zip(rows, perm)) for perm in itertools.permutations(range(1, delta + 1))])
+        best = None
+        for choice in itertools.product(*per_col):
+            O = np.zeros((m, m), dtype=np.int64)
+            for j, mp in enumerate(choice):
+                for i, v in mp.items():
+                    O[i, j] = v
+            qm = int(OA.Q(O).max())
+            best = qm if best is None else min(best, qm)
+        O = OO.chunk_ordering(S)
+        check_ordering(O, S)
+        assert OO.q_max(O) == best
+
+
+def pin_ordering_regular_graphs():
+    """Random regular supports and a random regular graph's adjacency: valid, optimal orderings;
+    the cyclic support gets the same Q_max as the cyclic order."""
+    g = rng(31)
+    for m, delta in [(10, 3), (50, 5), (64, 8)]:
+        S = _random_regular_support(g, m, delta)
+        check_ordering(OO.chunk_ordering(S), S)
+    from workloads import gen
+    A = gen.random_regular_graph(60, 6) != 0
+    check_ordering(OO.chunk_ordering(A), A)
+    C = OA.cyclic_O(12, 12, 3)
+    assert OO.q_max(OO.chunk_ordering(C != 0)) == OO.q_max(C)
+
+
+# ---------------------------------------------------------------------------
+# simulation (Sec. 4)
+# ---------------------------------------------------------------------------
+
+def pin_simulation_hand_example():
+    """Fig. 1(a)'s system (W_i holds D_i then D_{i+1}) with chunk times worked by hand:
+    W1: 1, 3 (finishes D1 at 1, D2 at 4); W2: 2, 2 (D2 at 2, D3 at 4); W3 failed.
+    ell = 1: D1 at 1, D2 at 2, D3 at 4 -> the protocol completes at 4; original GC needs
+    finished workers covering D1..D3: W1 (done at 4) covers D1, D2, W2 (done at 4) D2, D3 -> 4.
+    ell = 2: D1's copies are on W1 and W3 (failed) -> never."""
+    O = OA.cyclic_O(3, 3, 1)
+    tau = np.array([[[1.0, 3.0], [2.0, 2.0], [5.0, 5.0]]])
+    failed = np.array([[False, False, True]])
+    part, orig = OS.completion_times(tau, failed, O, 1)
+    assert part[0] == 4.0 and orig[0] == 4.0
+    part2, orig2 = OS.completion_times(tau, failed, O, 2)
+    assert np.isinf(part2[0]) and np.isinf(orig2[0])
+    tau_b = np.array([[[1.0, 3.0], [2.0, 2.0], [0.5, 9.0]]])       # W3 alive: D3 at 0.5
+    part, orig = OS.completion_times(tau_b, None, O, 1)
+    assert part[0] == 2.0 and orig[0] == 4.0                       # original waits for W1 or W2 to finish
+    psi = OS.progress(tau, failed, np.array([0.5, 1.0, 3.9, 4.0]))
+    assert psi[0].tolist() == [[0, 0, 0], [1, 0, 0], [1, 1, 0], [2, 2, 0]]
+
+
+def pin_simulation_grid_route():
+    """Second route: at every event time T (the only times the state changes), decide
+    decodability of psi(T) with the protocol's coverage; the first decodable one is the
+    completion time.  Original GC: psi_j = delta once worker j is done, else 0."""
+    g = rng(40)
+    for m, s, ell, nfail in [(6, 2, 1, 1), (8, 3, 2, 1), (10, 3, 3, 1), (7, 2, 1, 0)]:
+        O = OA.cyclic_O(m, m, s)
+        for _ in range(6):
+            tau = g.exponential(1.0, size=(1, m, s + 1))
+            failed = np.zeros((1, m), dtype=bool)
+            failed[0, g.choice(m, nfail, replace=False)] = True
+            part, orig = OS.completion_times(tau, failed, O, ell)
+            cum = np.cumsum(tau[0], axis=1)
+            times = np.unique(cum[~failed[0]].ravel())
+            psi_all = OS.progress(tau, failed, times)[0]
+            dec = [OP.decodable(O, psi_all[k], ell) for k in range(len(times))]
+            want = times[dec.index(True)] if any(dec) else np.inf
+            assert part[0] == want
+            fulls = np.unique(cum[~failed[0], -1])
+            dec_o = [OP.decodable(O, np.where((cum[:, -1] <= T) & ~failed[0], s + 1, 0), ell) for T in fulls]
+            want_o = fulls[dec_o.index(True)] if any(dec_o) else np.inf
+            assert orig[0] == want_o
+            assert part[0] <= orig[0]
+
+
 ALL_PINS = [
     pin_fig1a_ordering, pin_cyclic_invariants, pin_tables_roundtrip,
     pin_grad_at_zero, pin_grad_finite_difference, pin_grad_multi_point,
     pin_fig1a_motivation, pin_sec2_2_support, pin_sec2_2_closed_forms, pin_remark1_ell1,
     pin_ls_optimality, pin_coef_err_identity, pin_worker_agreement, pin_two_routes,
     pin_exact_recovery, pin_ell1_masked_sum, pin_compact_layout, pin_widen_bf16,
+    pin_ordering_bruteforce_optimum, pin_ordering_regular_graphs,
+    pin_simulation_hand_example, pin_simulation_grid_route,
 ]

@@ -121,3 +121,30 @@ def test_workspace_sizes():
     assert gcx.gc_reconstruct_workspace_size(10, 50, 1024, 1) == 0
     assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 4) == 0
     assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 128
+
+
+def test_assign_regular_algorithm2():
+    """gc_assign(GC_ASSIGN_REGULAR): Algorithm 2 in the library gives a valid, optimal ordering
+    (orderings are not unique; validity and Q_max are)."""
+    import pins
+    import oracle.ordering as OO
+    from workloads import gen
+    g = np.random.default_rng(5)
+    supports = [pins._random_regular_support(g, m, dl) for m, dl in [(4, 2), (10, 3), (50, 5), (97, 9)]]
+    supports.append(gen.random_regular_graph(200, 8) != 0)
+    supports.append(OA.cyclic_O(20, 20, 3) != 0)
+    for S in supports:
+        m, delta = S.shape[0], int(S.sum(axis=0)[0])
+        O, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_REGULAR, m, m, -1, S.astype(np.int32), delta, delta)
+        pins.check_ordering(O, S)
+        assert OO.q_max(O) == OO.q_max(OO.chunk_ordering(S))
+        o2, h2, p2 = OA.tables(O, delta, delta)
+        assert (order == o2).all() and (holder == h2).all() and (hpos == p2).all()
+
+
+def test_assign_regular_rejects_irregular():
+    S = np.eye(5, dtype=np.int32)
+    S[0, 1] = 1                                     # row 0 has degree 2
+    assert _raw_assign(gcx.GC_ASSIGN_REGULAR, 5, 5, -1, S, 1, 1) == gcx.GC_EINVAL
+    S2 = np.ones((4, 5), dtype=np.int32)          # N != m
+    assert _raw_assign(gcx.GC_ASSIGN_REGULAR, 4, 5, -1, S2, 5, 4) == gcx.GC_EINVAL

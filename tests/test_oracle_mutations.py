@@ -9,7 +9,9 @@ import pytest
 
 import oracle.assignment as OA
 import oracle.gradients as OG
+import oracle.ordering as OO
 import oracle.protocol as OP
+import oracle.simulation as OS
 import pins
 
 _orig_processed = OP.processed
@@ -84,6 +86,45 @@ def m_widen_low_half(G, dtype="f32"):
     return np.asarray(G, dtype=np.float64)
 
 
+_orig_ordering = OO.chunk_ordering
+
+
+def m_ordering_unweighted(A):
+    O = _orig_ordering(A)
+    return (O != 0).astype(np.int64)           # drops the weights i of O = sum_i i P_i
+
+
+def m_ordering_greedy(A):
+    # takes, for every chunk in turn, the first worker still free: not a matching step
+    S = np.asarray(A) != 0
+    N, m = S.shape
+    delta = int(S.sum(axis=0)[0])
+    O = np.zeros((N, m), dtype=np.int64)
+    for j in range(m):
+        rows = np.flatnonzero(S[:, j])
+        for t, i in enumerate(rows):
+            O[i, j] = t + 1
+    return O
+
+
+_orig_completion = OS.completion_time
+
+
+def m_completion_off_by_one(tau_r, failed_r, O, ell, full_only=False):
+    # stops at ell - 1 copies
+    return _orig_completion(tau_r, failed_r, O, max(1, ell - 1), full_only) if ell > 1 else \
+        _orig_completion(tau_r, failed_r, O, ell, not full_only)
+
+
+def m_progress_strict(tau, failed, T):
+    tau = np.asarray(tau, dtype=np.float64)
+    cum = np.cumsum(tau, axis=2)
+    psi = (cum[:, None, :, :] < np.asarray(T)[None, :, None, None]).sum(axis=3)
+    if failed is not None:
+        psi = np.where(np.asarray(failed, dtype=bool)[:, None, :], 0, psi)
+    return psi
+
+
 def m_grad_sign(Xi, yi, w, loss):
     Xi = np.asarray(Xi, dtype=np.float64)
     z = Xi @ np.asarray(w, dtype=np.float64)
@@ -118,6 +159,10 @@ MUTANTS = [
     (OA, "cyclic_O", m_cyclic_reversed),
     (OP, "compact", m_compact_shifted),
     (OP, "widen", m_widen_low_half),
+    (OO, "chunk_ordering", m_ordering_unweighted),
+    (OO, "chunk_ordering", m_ordering_greedy),
+    (OS, "completion_time", m_completion_off_by_one),
+    (OS, "progress", m_progress_strict),
     (OG, "chunk_gradient", m_grad_sign),
     (OG, "chunk_gradient", m_grad_no_sigmoid),
     (OG, "chunk_gradient", m_grad_residual_misindexed),

@@ -1,0 +1,122 @@
+"""GPU parity for regular-graph assignments (Algorithm 2) and the Sec. 4 simulation kernels.
+
+The assignment support is a random 8-regular graph on 200 vertices (the kind of
+expander the paper's approximate-GC experiments use); the oracle orders it with
+its own Algorithm 2 and the library receives that ordering through
+GC_ASSIGN_ORDER, so both sides see the same tables.
+"""
+from __future__ import annotations
+
+import functools
+
+import numpy as np
+import pytest
+
+import oracle.assignment as OA
+import oracle.ordering as OO
+import oracle.protocol as OP
+import oracle.simulation as OS
+import oracle_runs as R_
+from workloads import GRAPH, Workload, gen
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2405_19509_amd import gcx  # noqa: E402
+
+U = R_.U
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+@functools.lru_cache(maxsize=None)
+def graph_tables(m=GRAPH.m, nu=GRAPH.delta):
+    A = gen.random_regular_graph(m, nu)
+    O = OO.chunk_ordering(A)
+    _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, m, m, -1, O.astype(np.int32), nu, nu)
+    return O, order, holder, hpos
+
+
+@pytest.mark.parametrize("ell", [1, 2, 3])
+def test_graph_assignment_decode_encode_combine(ell):
+    wl = GRAPH
+    O, order, holder, hpos = graph_tables()
+    psi = gen.psi(wl, count=300)
+    R = gen.shared_R(wl.m, ell)
+    cov, dec, cerr, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+    cov, dec, cerr, Bc = host(cov), host(dec), host(cerr), host(Bc)
+    for p in range(len(psi)):
+        c = OP.coverage(O, psi[p])
+        assert (cov[p] == c).all() and dec[p] == int((c >= ell).all()) and cerr[p] == int(np.maximum(0, ell - c).sum())
+    sub = list(range(0, 300, 25))
+    Bc_ref, kappa = R_.coefficients(O, psi[sub], R)
+    assert (np.abs(Bc[sub].astype(np.float64) - Bc_ref) <= R_.bc_bound(Bc_ref, kappa, O)).all()
+    # encode + combine on identical inputs (oracle coefficients, given gradients)
+    G = gen.given_G(wl)
+    Bc32 = Bc_ref.astype(np.float32)
+    ps = psi[sub]
+    T = host(gcx.gc_encode(dev(G), dev(ps), dev(order), dev(Bc32)))
+    T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), ps, order, G, ell)
+    sent = ps > 0
+    assert (np.abs(T[sent] - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    T32 = T_ref.astype(np.float32)
+    gh, _ = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, psi=dev(ps))
+    gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, wl.d)
+    assert (np.abs(host(gh) - gh_ref) <= R_.gamma(wl.m) * mag).all()
+
+
+def test_progress_matches_oracle_bit_exact():
+    wl = GRAPH
+    tau, failed = gen.chunk_times(wl, 64)
+    T = np.linspace(0.0, 12.0, 49)
+    psi = host(gcx.gc_progress(dev(tau), dev(T), failed=dev(failed.astype(np.uint8))))
+    assert np.array_equal(psi, OS.progress(tau, failed, T))
+    psi_nf = host(gcx.gc_progress(dev(tau), dev(T)))
+    assert np.array_equal(psi_nf, OS.progress(tau, None, T))
+
+
+def test_coverage_only_decode_over_time_grid():
+    """The PS's view over time (the trigger policy): coefficient error sum_i max(0, ell - Delta_i)
+    of psi(T) for every (trial, deadline), from progress + coverage-only decode."""
+    wl = GRAPH
+    O, order, holder, hpos = graph_tables()
+    tau, failed = gen.chunk_times(wl, 16)
+    T = np.linspace(0.5, 16.0, 32)
+    psi = gcx.gc_progress(dev(tau), dev(T), failed=dev(failed.astype(np.uint8)))
+    flat = psi.reshape(-1, wl.m)
+    for ell in (1, 2, 3):
+        _, dec, cerr, Bc = gcx.gc_decode_coeffs(flat, dev(order), dev(holder), dev(hpos),
+                                               dev(gen.shared_R(wl.m, ell)), coverage_only=True)
+        assert Bc is None
+        ref_psi = OS.progress(tau, failed, T).reshape(-1, wl.m)
+        cerr, dec = host(cerr), host(dec)
+        for a in range(len(ref_psi)):
+            assert cerr[a] == OP.coef_err(O, ref_psi[a], ell)
+            assert dec[a] == int(OP.decodable(O, ref_psi[a], ell))
+
+
+@pytest.mark.parametrize("kind", ["cyclic", "graph"])
+def test_completion_times_bit_exact(kind):
+    """Exact-GC completion time of the proposed protocol and of original GC, N = m = 200,
+    delta = 8, alpha = delta - ell failed workers (the exact-GC simulation setup of Sec. 4)."""
+    if kind == "cyclic":
+        wl = Workload(name="cyclic_m200_d8", N=200, m=200, s=7, d=16, P=1, ells=(1,))
+        O = OA.cyclic_O(200, 200, 7)
+        _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, 200, 200, 7)
+    else:
+        wl = GRAPH
+        O, order, holder, hpos = graph_tables()
+    for ell in (1, 2, 4, 7):
+        tau, failed = gen.chunk_times(wl, 40, seed=ell, failed=wl.delta - ell)
+        part, orig = gcx.gc_completion_times(dev(tau), dev(holder), dev(hpos), ell,
+                                             failed=dev(failed.astype(np.uint8)))
+        p_ref, o_ref = OS.completion_times(tau, failed, O, ell)
+        assert np.array_equal(host(part), p_ref) and np.array_equal(host(orig), o_ref)
+        assert (p_ref <= o_ref).all()

@@ -36,6 +36,8 @@ class Workload:
     forced_zero: int = 0        # workers forced to psi = 0 per pattern
     ls_forced_zero: int = 0     # extra forced zeros of the least-squares run
     ls_ells: Tuple[int, ...] = field(default_factory=tuple)
+    assignment: str = "cyclic"  # "cyclic" | "regular_graph" (random nu-regular graph, nu = s + 1)
+    deadline: float = 0.0       # fixed deadline of the "fail_exp_deadline" pattern model
 
     @property
     def delta(self) -> int:
@@ -74,5 +76,13 @@ LARGE = Workload(name="given_m200_d16M_bf16", N=200, m=200, s=19, d=1 << 24,
                  P=100000, ells=(1, 2), g_dtype="bf16", pattern="hetero_median",
                  ls_forced_zero=100, ls_ells=(1, 2, 4))
 
+# Regular-graph assignment of the paper's approximate-GC experiments: a random
+# 8-regular graph on m = 200 vertices as the support, ordered by Algorithm 2;
+# nu - 1 = 7 failed workers, Exp(1) chunk times, deadline T.
+GRAPH = Workload(name="graph_m200_nu8", N=200, m=200, s=7, d=4096, P=2000, ells=(1, 2, 3),
+                 g_dtype="f32", pattern="fail_exp_deadline", forced_zero=7,
+                 assignment="regular_graph", deadline=6.0)
+
 ALL = (TINY, SMALL, HEADLINE, BANDWIDTH, LARGE)
-BY_NAME = {w.name: w for w in ALL}
+EXTRA = (GRAPH,)
+BY_NAME = {w.name: w for w in ALL + EXTRA}

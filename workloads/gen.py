@@ -10,6 +10,7 @@ so that changing one size never changes another quantity's values:
     spawn key (4,)     R   (the shared ell x m Gaussian matrix)
     spawn key (5, 0)   per-worker speed factors (heterogeneous model)
     spawn key (5, 1+b) straggler patterns of batch b (PATTERN_BATCH patterns)
+    spawn key (6, m, nu) random nu-regular graphs on m vertices (regular-graph assignments)
 
 Straggler patterns follow the simulation model of the paper's numerical
 section: a worker processes its chunks in its fixed order, one chunk at a time,
@@ -183,6 +184,12 @@ def _pattern_batch(wl: Workload, b: int, Pb: int, variant: str, seed: int) -> np
         cum = np.cumsum(tau, axis=2)
         T = delta + gammaincinv(delta, 0.5)
         return _finished_by(cum, np.full(Pb, T))
+    if wl.pattern == "fail_exp_deadline":
+        forced = np.argsort(rng.random((Pb, m)), axis=1)[:, :wl.forced_zero]
+        tau = rng.exponential(1.0, size=(Pb, m, delta))
+        psi = _finished_by(np.cumsum(tau, axis=2), np.full(Pb, wl.deadline))
+        np.put_along_axis(psi, forced, 0, axis=1)
+        return psi
     if wl.pattern == "hetero_median":
         speed = worker_speeds(wl, seed)
         tau = rng.exponential(1.0, size=(Pb, m, delta)) / speed[None, :, None]
@@ -215,3 +222,59 @@ def psi(wl: Workload, seed: int = 0, start: int = 0, count=None, variant: str = 
         out[p - start:p - start + hi - lo] = batch[lo:hi]
         p = b0 + hi
     return out
+
+
+# ---------------------------------------------------------------------------
+# random regular graphs (assignment supports of the regular-graph experiments)
+# ---------------------------------------------------------------------------
+
+def random_regular_graph(m: int, nu: int, seed: int = 0, attempt_limit: int = 1000) -> np.ndarray:
+    """Adjacency matrix [m][m] (0/1, symmetric, zero diagonal) of a random nu-regular simple graph.
+
+    Stubs are paired one random pair at a time among the pairs that create no loop
+    and no repeated edge; a dead end restarts the pairing (the Steger-Wormald
+    procedure).  Used as the assignment support A (chunk i on worker j iff edge ij),
+    the kind of expander-based assignment of the paper's approximate-GC experiments.
+    """
+    if (m * nu) % 2 or nu >= m:
+        raise ValueError("need m * nu even and nu < m")
+    rng = _rng(seed, 6, m, nu)
+    for _ in range(attempt_limit):
+        A = np.zeros((m, m), dtype=np.int8)
+        stubs = np.repeat(np.arange(m), nu)
+        rng.shuffle(stubs)
+        stubs = list(stubs)
+        ok = True
+        while stubs:
+            placed = False
+            for _try in range(50):
+                a = int(rng.integers(len(stubs)))
+                b = int(rng.integers(len(stubs)))
+                u, v = stubs[a], stubs[b]
+                if a != b and u != v and not A[u, v]:
+                    A[u, v] = A[v, u] = 1
+                    for k in sorted((a, b), reverse=True):
+                        stubs[k] = stubs[-1]
+                        stubs.pop()
+                    placed = True
+                    break
+            if not placed:
+                ok = False
+                break
+        if ok:
+            return A
+    raise RuntimeError("no simple regular graph found")
+
+
+def chunk_times(wl: Workload, trials: int, seed: int = 0, failed: int | None = None):
+    """The paper's simulation model, for time sweeps: per-chunk times tau [trials][m][delta]
+    ~ i.i.d. Exp(1) (fp64) and a failure mask [trials][m] with `failed` workers chosen
+    uniformly at random per trial (they never finish a chunk)."""
+    rng = _rng(seed, 7, trials, wl.m)
+    k = wl.forced_zero if failed is None else failed
+    fail = np.zeros((trials, wl.m), dtype=bool)
+    if k:
+        idx = np.argsort(rng.random((trials, wl.m)), axis=1)[:, :k]
+        np.put_along_axis(fail, idx, True, axis=1)
+    tau = rng.exponential(1.0, size=(trials, wl.m, wl.delta))
+    return tau, fail
