@@ -226,6 +226,21 @@ int gc_completion_times(const double *tau, const uint8_t *failed, int64_t R, int
                         int32_t gamma, int32_t ell, double *partial, double *original,
                         hipStream_t stream);
 
+/*
+ * gc_original_ls -- original GC's approximate decoding, the comparison of Sec. 4:
+ * with F the workers that have processed all their chunks (psi[p][j] equal to
+ * the worker's load), r = argmin ||A_F r - 1||_2 over the 0/1 assignment
+ * support A (r_j = 0 outside F), and err[p] = ||A r - 1||^2.  Solved per
+ * pattern by CGLS in fp64 from r = 0 (so the minimum-norm solution when A_F is
+ * rank deficient), stopping when ||A_F^T (1 - A_F r)|| <= tol times its
+ * initial value or after max_iter iterations (iters[p] = iterations used;
+ * iters may be NULL).  psi [P][m], order [m][delta], holder [N][gamma] int32,
+ * err [P] fp64: all device.  Requires N, m <= GC_MAX_M.
+ */
+int gc_original_ls(const int32_t *psi, int64_t P, int32_t N, int32_t m, const int32_t *order,
+                   int32_t delta, const int32_t *holder, int32_t gamma, int32_t max_iter,
+                   double tol, double *err, int32_t *iters, hipStream_t stream);
+
 size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell);
 int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
                    int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,

@@ -65,3 +65,20 @@ def completion_times(tau: np.ndarray, failed: np.ndarray | None, O: np.ndarray, 
     part = np.array([completion_time(tau[r], f[r], O, ell) for r in range(R)])
     orig = np.array([completion_time(tau[r], f[r], O, ell, full_only=True) for r in range(R)])
     return part, orig
+
+
+def original_ls_error(O: np.ndarray, psi: np.ndarray) -> float:
+    """Original GC's approximate decoding (the comparison of Sec. 4): with F the workers
+    that have processed all their chunks, r = argmin ||A_F r - 1||_2 (r_j = 0 outside F),
+    A the 0/1 assignment support; returns the squared residual ||A r - 1||^2."""
+    O = np.asarray(O)
+    psi = np.asarray(psi)
+    A = (O != 0).astype(np.float64)
+    loads = A.sum(axis=0)
+    F = np.flatnonzero((psi >= loads) & (loads > 0))
+    ones = np.ones(A.shape[0])
+    if len(F) == 0:
+        return float(A.shape[0])
+    r = np.linalg.lstsq(A[:, F], ones, rcond=None)[0]
+    res = A[:, F] @ r - ones
+    return float(res @ res)

@@ -42,6 +42,7 @@ SIGNATURES = {
     "gc_encode": (_c.c_int, [_p, _i32, _i32, _i64, _p, _p, _p, _i64, _i32, _i32, _i32, _p, _p]),
     "gc_progress": (_c.c_int, [_p, _p, _i64, _i32, _i32, _p, _i32, _p, _p]),
     "gc_completion_times": (_c.c_int, [_p, _p, _i64, _i32, _i32, _i32, _p, _p, _i32, _i32, _p, _p, _p]),
+    "gc_original_ls": (_c.c_int, [_p, _i64, _i32, _i32, _p, _i32, _p, _i32, _i32, _c.c_double, _p, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
 }
@@ -303,3 +304,24 @@ def gc_completion_times(tau, holder, hpos, ell: int, failed=None, partial=None, 
         _stream(stream))
     _check("gc_completion_times", st)
     return partial, original
+
+
+def gc_original_ls(psi, order, holder, max_iter: int = 1000, tol: float = 1e-12, err=None,
+                   iters=None, stream=None):
+    """psi [P][m] int32, tables -> (err [P] fp64, iters [P] int32): original GC's
+    least-squares error over the fully finished workers."""
+    torch = _torch()
+    P, m = psi.shape
+    _, delta = order.shape
+    N, gamma = holder.shape
+    if err is None:
+        err = torch.empty(P, dtype=torch.float64, device=psi.device)
+    if iters is None:
+        iters = torch.empty(P, dtype=torch.int32, device=psi.device)
+    st = load().gc_original_ls(_dev(psi, "psi", torch.int32), P, N, m,
+                               _dev(order, "order", torch.int32, (m, delta)), delta,
+                               _dev(holder, "holder", torch.int32, (N, gamma)), gamma, max_iter, tol,
+                               _dev(err, "err", torch.float64, (P,)),
+                               _dev(iters, "iters", torch.int32, (P,)), _stream(stream))
+    _check("gc_original_ls", st)
+    return err, iters

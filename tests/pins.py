@@ -564,6 +564,32 @@ def pin_simulation_grid_route():
             assert part[0] <= orig[0]
 
 
+def pin_original_ls():
+    """Original GC's least-squares error: closed forms and a projection identity.
+    No finished worker: N.  One finished worker of load delta: N - delta.  Finished workers
+    whose supports partition the chunks: 0.  In general ||(I - Q Q^T) 1||^2 for an
+    orthonormal basis Q of range(A_F) (QR, a different routine than the oracle's lstsq)."""
+    O = OA.cyclic_O(6, 6, 1)                      # worker j holds chunks j, j+1
+    assert OS.original_ls_error(O, np.zeros(6)) == 6.0
+    assert abs(OS.original_ls_error(O, np.array([2, 0, 0, 0, 0, 0])) - 4.0) < 1e-12
+    assert abs(OS.original_ls_error(O, np.array([2, 0, 2, 0, 2, 0]))) < 1e-12   # {0,1},{2,3},{4,5}
+    g = rng(41)
+    from workloads import gen
+    A = gen.random_regular_graph(30, 4) != 0
+    O2 = OO.chunk_ordering(A)
+    for _ in range(20):
+        psi = g.integers(0, 5, size=30)
+        F = np.flatnonzero(psi >= 4)
+        want = 30.0
+        if len(F):
+            Q, Rr = np.linalg.qr(A[:, F].astype(float))
+            keep = np.abs(np.diag(Rr)) > 1e-10
+            Q = Q[:, keep]
+            v = np.ones(30) - Q @ (Q.T @ np.ones(30))
+            want = float(v @ v)
+        assert abs(OS.original_ls_error(O2, psi) - want) < 1e-9
+
+
 ALL_PINS = [
     pin_fig1a_ordering, pin_cyclic_invariants, pin_tables_roundtrip,
     pin_grad_at_zero, pin_grad_finite_difference, pin_grad_multi_point,
@@ -571,5 +597,5 @@ ALL_PINS = [
     pin_ls_optimality, pin_coef_err_identity, pin_worker_agreement, pin_two_routes,
     pin_exact_recovery, pin_ell1_masked_sum, pin_compact_layout, pin_widen_bf16,
     pin_ordering_bruteforce_optimum, pin_ordering_regular_graphs,
-    pin_simulation_hand_example, pin_simulation_grid_route,
+    pin_simulation_hand_example, pin_simulation_grid_route, pin_original_ls,
 ]

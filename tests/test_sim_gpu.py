@@ -120,3 +120,21 @@ def test_completion_times_bit_exact(kind):
         p_ref, o_ref = OS.completion_times(tau, failed, O, ell)
         assert np.array_equal(host(part), p_ref) and np.array_equal(host(orig), o_ref)
         assert (p_ref <= o_ref).all()
+
+
+@pytest.mark.parametrize("kind", ["cyclic", "graph"])
+def test_original_ls_matches_oracle(kind):
+    """Original GC's least-squares error over the fully finished workers, against lstsq."""
+    if kind == "cyclic":
+        O = OA.cyclic_O(50, 50, 4)
+        _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, 50, 50, 4)
+        from workloads import HEADLINE
+        psi = gen.psi(HEADLINE, count=200)
+    else:
+        O, order, holder, hpos = graph_tables()
+        psi = gen.psi(GRAPH, count=200)
+    err, iters = gcx.gc_original_ls(dev(psi), dev(order), dev(holder))
+    err, iters = host(err), host(iters)
+    ref = np.array([OS.original_ls_error(O, p) for p in psi])
+    assert (np.abs(err - ref) <= 1e-9 * np.maximum(1.0, ref)).all(), np.abs(err - ref).max()
+    assert iters.max() < 1000
