@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--experiment", choices=["hotpath", "completion", "trigger"], default="hotpath",
+                    help="hotpath: the headline step (default); completion: exact-GC completion times, "
+                         "proposed vs original GC; trigger: error vs deadline, proposed vs original GC")
+    ap.add_argument("--trials", type=int, default=1000)
     ap.add_argument("--mfma-points", type=int, default=256,
                     help="also time the chunk gradients at this many evaluation points (matrix-core "
                          "path; 0 = skip); reported under 'mfma', outside the step")
@@ -150,12 +154,109 @@ def cpu_baseline(wl, ell, X, y, w, psi, R, budget_s):
     }
 
 
+def _tables(gcx, kind, m, nu):
+    """Cyclic or regular-graph (Algorithm 2 in the library) assignment tables for m = N."""
+    from workloads import gen
+    if kind == "cyclic":
+        return gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, m, m, nu - 1)
+    A = gen.random_regular_graph(m, nu).astype(np.int32)
+    return gcx.gc_assign(gcx.GC_ASSIGN_REGULAR, m, m, -1, A, nu, nu)
+
+
+def experiment_completion(args):
+    """Exact-GC completion time (Sec. 4): cyclic N = m = 200 with delta = 8, and a random
+    8-regular graph; alpha = delta - ell failed workers; Exp(1) chunk times."""
+    import torch
+
+    from paper_2405_19509_amd import gcx
+    from workloads import GRAPH, Workload, gen
+    dev = torch.device("cuda:0")
+    out = {"metric": "exact-GC completion time, proposed vs original GC (simulated time units)",
+           "unit": "trials/s", "n_gpus": 1, "higher_is_better": True, "data": "synthetic",
+           "config": {"workload": "completion_m200_delta8", "m": 200, "delta": 8, "trials": args.trials,
+                      "failures": "delta - ell", "chunk_times": "Exp(1)"}, "results": {}}
+    total_ms, total_trials = 0.0, 0
+    for kind in ("cyclic", "graph"):
+        O, order, holder, hpos = _tables(gcx, kind, 200, 8)
+        hd, pd = torch.from_numpy(holder).to(dev), torch.from_numpy(hpos).to(dev)
+        rows = {}
+        for ell in range(1, 8):
+            wl = Workload(name="c", N=200, m=200, s=7, d=1, P=1, ells=(ell,)) if kind == "cyclic" else GRAPH
+            tau, failed = gen.chunk_times(wl, args.trials, seed=100 + ell, failed=8 - ell)
+            taud, fd = torch.from_numpy(tau).to(dev), torch.from_numpy(failed.astype(np.uint8)).to(dev)
+            gcx.gc_completion_times(taud, hd, pd, ell, failed=fd)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            part, orig = gcx.gc_completion_times(taud, hd, pd, ell, failed=fd)
+            e1.record()
+            torch.cuda.synchronize()
+            total_ms += e0.elapsed_time(e1)
+            total_trials += args.trials
+            p, o = part.cpu().numpy(), orig.cpu().numpy()
+            rows[str(ell)] = {"proposed_mean": float(p.mean()), "original_mean": float(o.mean()),
+                              "proposed_std": float(p.std()), "original_std": float(o.std()),
+                              "ratio": float(o.mean() / p.mean())}
+        out["results"][kind] = rows
+    out["value"] = total_trials / (total_ms * 1e-3)
+    out["paper_context"] = ("Sec. 4: proposed protocol about 2x faster than original GC for exact recovery "
+                            "(cyclic N = m = 200, delta = 8, and graph G1; alpha = delta - ell; Exp(1)); "
+                            "original GC on G1 at ell = 1 about 6 time units")
+    print(json.dumps(out))
+
+
+def experiment_trigger(args):
+    """Error vs deadline T on a random 8-regular graph (m = 200), alpha = 7 failures:
+    the proposed protocol's coefficient error sum_i max(0, ell - Delta_i) (equal to its
+    least-squares residual, Sec. 2.1) for ell = 1, 2, 3, and original GC's least-squares
+    error over fully finished workers (ell = 1)."""
+    import torch
+
+    from paper_2405_19509_amd import gcx
+    from workloads import GRAPH, gen
+    dev = torch.device("cuda:0")
+    O, order, holder, hpos = _tables(gcx, "graph", 200, 8)
+    od, hd, pd = (torch.from_numpy(a).to(dev) for a in (order, holder, hpos))
+    T = np.arange(0.0, 24.01, 1.0)
+    tau, failed = gen.chunk_times(GRAPH, args.trials, seed=7)
+    taud, fd, Td = (torch.from_numpy(a).to(dev) for a in (tau, failed.astype(np.uint8), T))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    psi = gcx.gc_progress(taud, Td, failed=fd).reshape(-1, 200)
+    curves = {}
+    for ell in (1, 2, 3):
+        _, _, cerr, _ = gcx.gc_decode_coeffs(psi, od, hd, pd, torch.from_numpy(gen.shared_R(200, ell)).to(dev),
+                                             coverage_only=True)
+        curves[f"proposed_ell{ell}"] = cerr
+    err_o, iters = gcx.gc_original_ls(psi, od, hd)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    res = {k: v.view(args.trials, len(T)).double().mean(0).cpu().numpy().tolist() for k, v in curves.items()}
+    res["original_ell1"] = err_o.view(args.trials, len(T)).mean(0).cpu().numpy().tolist()
+    out = {"metric": "coefficient-space error vs deadline, proposed (ell=1,2,3) vs original GC (ell=1)",
+           "unit": "(trial, deadline) patterns/s", "value": args.trials * len(T) / (ms * 1e-3), "n_gpus": 1,
+           "higher_is_better": True, "data": "synthetic",
+           "config": {"workload": "trigger_graph_m200_nu8", "m": 200, "nu": 8, "failures": 7,
+                      "trials": args.trials, "deadlines": T.tolist()},
+           "results": res, "max_cgls_iters": int(iters.max().item()),
+           "paper_context": ("Sec. 4, Fig. 3(a): on G1 (m = 200, nu = 8, alpha = 7) the proposed protocol's "
+                             "MSE is several orders of magnitude below original GC's as T grows, also for "
+                             "ell >= 2; its estimate (ell - Delta)/ell per column tracks the error")}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the hot path is one GPU's share; got --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    if args.experiment == "completion":
+        return experiment_completion(args)
+    if args.experiment == "trigger":
+        return experiment_trigger(args)
     import torch
 
     from paper_2405_19509_amd import gcx
