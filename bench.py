@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--mfma-points", type=int, default=256,
                     help="also time the chunk gradients at this many evaluation points (matrix-core "
                          "path; 0 = skip); reported under 'mfma', outside the step")
+    ap.add_argument("--no-direct", dest="direct", action="store_false",
+                    help="skip timing gc_decode_direct (reported under 'direct', outside the step)")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of a plain device copy run once before warm-up (counter calibration)")
     return ap.parse_args()
@@ -115,6 +117,39 @@ def time_many_points(gcx, wl, Xd, yd, b, dev, reps=5):
     return {"bound": "mfma", "points": b, "ms": ms, "achieved": tf, "peak": FP32_MFMA_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": tf / FP32_MFMA_PEAK_TFLOPS, "dtype": "f32",
             "note": "gc_chunk_grads with W [b][d]: Z = X W^T, residuals, G = U^T X per chunk"}
+
+
+def time_direct(gcx, wl, ell, G, gsum, psid, orderd, holderd, hposd, Rd, ghat, sqerr, reps=10):
+    """gc_decode_direct on the step's own inputs: the same estimates and squared errors without
+    the workers' transmitted vectors.  A dense fp32 contraction of the per-pattern mixing rows
+    [P ell][N ell] with the block-split gradients [N ell][L]: 2 P ell N ell L flops, reported
+    against the fp32 MFMA peak (time of the whole call: mixing matrices, contraction, error sums)."""
+    import torch
+    P = psid.shape[0]
+    ws = torch.empty(gcx.gc_decode_direct_workspace_size(P, wl.N, wl.d, ell), dtype=torch.uint8,
+                     device=G.device)
+
+    def call():
+        gcx.gc_decode_direct(G, psid, orderd, holderd, hposd, Rd, ghat=ghat, gsum=gsum, sqerr=sqerr,
+                             workspace=ws)
+    call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    L = -(-wl.d // ell)
+    flops = 2.0 * P * ell * wl.N * ell * L
+    tf = flops / (ms * 1e-3) / 1e12
+    del ws
+    return {"bound": "mfma", "ms": ms, "patterns_per_s": P / (ms * 1e-3), "achieved": tf,
+            "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tf / FP32_MFMA_PEAK_TFLOPS,
+            "flops": flops, "dtype": "f32", "ghat": True,
+            "note": "gc_decode_direct: estimate of every pattern from the chunk gradients through "
+                    "M_i = R[:, S_i] pinv(R[:, S_i]), outside the step"}
 
 
 def cpu_baseline(wl, ell, X, y, w, psi, R, budget_s):
@@ -369,6 +404,11 @@ def main():
                     "mse_vs_sum_g": float(se.mean() / wl.d),
                     "mse_decodable": float(se[decs == 1].mean() / wl.d) if (decs == 1).any() else None},
     }
+    if args.direct:
+        out["direct"] = time_direct(gcx, wl, ell, G, gsum, psid, orderd, holderd, hposd, Rd, ghat, sqerr)
+        # both routes give the same squared errors (up to fp32 rounding of the estimates)
+        se_d = sqerr.cpu().numpy()
+        out["direct"]["sqerr_max_abs_diff_vs_step"] = float(np.abs(np.sqrt(se_d) - np.sqrt(se)).max())
     if args.mfma_points > 0:
         out["mfma"] = time_many_points(gcx, wl, Xd, yd, args.mfma_points, dev)
     if not args.no_cpu_baseline:

@@ -11,6 +11,9 @@
  *   gc_decode_coeffs  coverage, decodability and Algorithm 1    (Sec. 2; Sec. 2.1)
  *   gc_encode         each worker's transmitted vector g_beta   (Sec. 2)
  *   gc_reconstruct    the PS combine  sum_j R[k][j] g_j         (Sec. 2.2)
+ *   gc_decode_direct  the same estimate without forming g_j     (Sec. 2; Sec. 2.2)
+ *   gc_progress, gc_completion_times, gc_original_ls
+ *                     the straggler simulations of Sec. 4
  *
  * Conventions (every entry point):
  *   - Row-major arrays, 0-based indices.  Chunk i is the paper's D_{i+1},
@@ -196,6 +199,37 @@ int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_
  * (it holds per-slice partial sums, reduced in a fixed order, so sqerr is
  * deterministic).
  */
+size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell);
+int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
+                   int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * gc_decode_direct -- the same estimate as gc_decode_coeffs + gc_encode +
+ * gc_reconstruct, computed at the PS without forming what the workers transmit.
+ * Putting the worker encode (Sec. 2) into the combine (Sec. 2.2) gives
+ *   block k of ghat[p] = sum_i sum_k' M_i[k][k'] * block k' of g_i,
+ *   M_i = R[:, S_i] B^(i)[S_i, :] = R[:, S_i] pinv(R[:, S_i]),
+ * the identity when Delta_i >= ell, the orthogonal projector onto the range of
+ * R[:, S_i] when 0 < Delta_i < ell, and zero when Delta_i = 0 (S_i, Delta_i as
+ * in gc_decode_coeffs, Sec. 2.1).  The mixing matrices are formed in fp64 and
+ * rounded once to fp32; the sum over chunks is an fp32 matrix-core contraction.
+ * A simulation shortcut only: in the protocol the PS never sees the g_i.
+ * G [N][d] (g_dtype GC_F32 or GC_BF16 bits), psi [P][m], holder/hpos
+ * [N][gamma] (gc_assign), R [ell][m]: device.  Outputs as in gc_reconstruct:
+ * ghat [P][d] fp32 (may be NULL), and with gsum [d] non-NULL, sqerr [P] fp64
+ * (may be NULL; deterministic).  At least one of ghat, sqerr.  workspace:
+ * device, 16-byte aligned, at least gc_decode_direct_workspace_size(P, N, d,
+ * ell) bytes.  Rows of psi must be valid (0 <= psi[p][j] <= load of j).
+ * Requires N, m <= GC_MAX_M.
+ */
+size_t gc_decode_direct_workspace_size(int64_t P, int32_t N, int64_t d, int32_t ell);
+int gc_decode_direct(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_t *psi,
+                     int64_t P, int32_t m, int32_t delta, const int32_t *holder,
+                     const int32_t *hpos, int32_t gamma, const float *R, int32_t ell,
+                     float *ghat, const float *gsum, double *sqerr, void *workspace,
+                     size_t workspace_bytes, hipStream_t stream);
+
 /*
  * gc_progress -- the straggler simulation of Sec. 4 at a grid of deadlines:
  * worker j finishes the chunk at position t of its order at time
@@ -240,11 +274,6 @@ int gc_completion_times(const double *tau, const uint8_t *failed, int64_t R, int
 int gc_original_ls(const int32_t *psi, int64_t P, int32_t N, int32_t m, const int32_t *order,
                    int32_t delta, const int32_t *holder, int32_t gamma, int32_t max_iter,
                    double tol, double *err, int32_t *iters, hipStream_t stream);
-
-size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell);
-int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
-                   int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
-                   void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -45,6 +45,9 @@ SIGNATURES = {
     "gc_original_ls": (_c.c_int, [_p, _i64, _i32, _i32, _p, _i32, _p, _i32, _i32, _c.c_double, _p, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
+    "gc_decode_direct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
+    "gc_decode_direct": (_c.c_int, [_p, _i32, _i32, _i64, _p, _i64, _i32, _i32, _p, _p, _i32, _p,
+                                    _i32, _p, _p, _p, _p, _sz, _p]),
 }
 
 _lib = None
@@ -268,6 +271,41 @@ def gc_reconstruct(T, R, d: int, psi=None, ghat=None, gsum=None, sqerr=None, wan
         _dev(sqerr, "sqerr", torch.float64, (P,)) if sqerr is not None else None,
         ws_ptr, ws_bytes, _stream(stream))
     _check("gc_reconstruct", st)
+    return ghat, sqerr
+
+
+def gc_decode_direct_workspace_size(P: int, N: int, d: int, ell: int) -> int:
+    return int(load().gc_decode_direct_workspace_size(P, N, d, ell))
+
+
+def gc_decode_direct(G, psi, order, holder, hpos, R, ghat=None, gsum=None, sqerr=None,
+                     want_ghat: bool = True, workspace=None, stream=None):
+    """G [N][d] (fp32 or bf16), psi [P][m], tables from gc_assign, R [ell][m] ->
+    (ghat [P][d] or None, sqerr [P] fp64 or None): the estimate of gc_reconstruct formed from
+    the chunk gradients directly.  sqerr is computed when gsum [d] is given."""
+    torch = _torch()
+    N, d = G.shape
+    P, m = psi.shape
+    ell = R.shape[0]
+    delta = order.shape[1]
+    gamma = holder.shape[1]
+    dv = G.device
+    if want_ghat and ghat is None:
+        ghat = torch.empty((P, d), dtype=torch.float32, device=dv)
+    if gsum is not None and sqerr is None:
+        sqerr = torch.empty(P, dtype=torch.float64, device=dv)
+    need = gc_decode_direct_workspace_size(P, N, d, ell)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dv)
+    st = load().gc_decode_direct(
+        _dev(G, "G", G.dtype), _g_dtype(G), N, d, _dev(psi, "psi", torch.int32, (P, m)), P, m, delta,
+        _dev(holder, "holder", torch.int32, (N, gamma)), _dev(hpos, "hpos", torch.int32, (N, gamma)),
+        gamma, _dev(R, "R", torch.float32, (ell, m)), ell,
+        _dev(ghat, "ghat", torch.float32, (P, d)) if ghat is not None else None,
+        _dev(gsum, "gsum", torch.float32, (d,)) if gsum is not None else None,
+        _dev(sqerr, "sqerr", torch.float64, (P,)) if sqerr is not None else None,
+        _dev(workspace, "workspace", torch.uint8), workspace.numel(), _stream(stream))
+    _check("gc_decode_direct", st)
     return ghat, sqerr
 
 

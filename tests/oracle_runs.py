@@ -125,3 +125,32 @@ def sampled_blocks(G, dtype, ell, xs):
             if c < d:
                 Gsub[:, k * S + s_] = OP.widen(G[:, c], dtype)
     return Gsub
+
+
+def mixing(O, psi, R):
+    """M [N][ell][ell] fp64 with M_i = R B^(i): how chunk i's blocks enter the estimate, from the
+    oracle's coefficients (``reconstruct_by_chunks`` sums M_i applied to g_i's blocks)."""
+    R = np.asarray(R, dtype=np.float64)
+    ell = R.shape[0]
+    B = OP.encoding_matrix_per_chunk(O, psi, R)
+    N = O.shape[0]
+    return np.stack([R @ B[:, i * ell:(i + 1) * ell] for i in range(N)])
+
+
+def direct_ref(O, psi, R, G):
+    """The estimate sum_i M_i g_i (fp64) of each pattern, with sum_i |M_i| |g_i| for its error
+    bound and the largest condition number of an R[:, S_i] with 0 < Delta_i < ell."""
+    R = np.asarray(R, dtype=np.float64)
+    ell = R.shape[0]
+    G = np.asarray(G, dtype=np.float64)
+    d = G.shape[1]
+    Gb = gblocks(G, ell)                                             # [N][ell][L]
+    out, mag, kap = [], [], []
+    for p in psi:
+        M = mixing(O, p, R)
+        out.append(np.einsum("ikq,iql->kl", M, Gb).reshape(-1)[:d])
+        mag.append(np.einsum("ikq,iql->kl", np.abs(M), np.abs(Gb)).reshape(-1)[:d])
+        c = OP.coverage(O, p)
+        k = [np.linalg.cond(R[:, S]) for S, n in zip(OP.processed_sets(O, p), c) if 0 < n < ell]
+        kap.append(max(k + [1.0]))
+    return np.stack(out), np.stack(mag), np.array(kap)

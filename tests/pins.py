@@ -350,6 +350,30 @@ def pin_two_routes():
             assert np.abs(a - b).max() < 1e-12 * max(1.0, np.abs(b).max())
 
 
+def pin_mixing_projector():
+    """What chunk i contributes to the estimate is M_i = R B^(i) applied to its blocks.  With B
+    from the workers' own solves (Algorithm 1), M_i must be the orthogonal projector onto the
+    range of R[:, S_i]: the identity once Delta_i >= ell (Gaussian R has full rank), zero when
+    Delta_i = 0, and Q Q^T from a QR factorisation of R[:, S_i] in between (Sec. 2.1, Sec. 2.2)."""
+    g = rng(19)
+    for m, s, ell in [(6, 2, 2), (6, 2, 3), (8, 3, 3), (9, 2, 4), (7, 4, 5)]:
+        O = OA.cyclic_O(m, m, s)
+        for psi in _random_patterns(g, m, s, 8):
+            R = g.standard_normal((ell, m))
+            B = OP.encoding_matrix(O, psi, R)
+            for i, S in enumerate(OP.processed_sets(O, psi)):
+                M = R @ B[:, i * ell:(i + 1) * ell]
+                if len(S) == 0:
+                    ref = np.zeros((ell, ell))
+                else:
+                    Q, _ = np.linalg.qr(R[:, S])
+                    Q = Q[:, :min(len(S), ell)]
+                    ref = Q @ Q.T
+                assert np.abs(M - ref).max() < 1e-9, (m, s, ell, psi, i)
+                if len(S) >= ell:
+                    assert np.abs(M - np.eye(ell)).max() < 1e-9
+
+
 # ---------------------------------------------------------------------------
 # encode + combine
 # ---------------------------------------------------------------------------
@@ -595,6 +619,7 @@ ALL_PINS = [
     pin_grad_at_zero, pin_grad_finite_difference, pin_grad_multi_point,
     pin_fig1a_motivation, pin_sec2_2_support, pin_sec2_2_closed_forms, pin_remark1_ell1,
     pin_ls_optimality, pin_coef_err_identity, pin_worker_agreement, pin_two_routes,
+    pin_mixing_projector,
     pin_exact_recovery, pin_ell1_masked_sum, pin_compact_layout, pin_widen_bf16,
     pin_ordering_bruteforce_optimum, pin_ordering_regular_graphs,
     pin_simulation_hand_example, pin_simulation_grid_route, pin_original_ls,

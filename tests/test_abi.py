@@ -106,6 +106,19 @@ def test_device_calls_validate_on_the_host():
     assert lib.gc_reconstruct(p, p, p, 4, 6, 64, 0, p, None, None, None, 0, None) == E         # ell = 0
     assert lib.gc_reconstruct(p, p, p, 4, 6, 64, 1, p, None, p, None, 0, None) == E            # sqerr w/o gsum
     assert lib.gc_reconstruct(p, p, None, 4, 6, 1 << 20, 1, None, p, p, None, 0, None) == E    # workspace
+    ws = gcx.gc_decode_direct_workspace_size(4, 6, 64, 1)
+    args = dict(G=p, g_dtype=0, N=6, d=64, psi=p, P=4, m=6, delta=3, holder=p, hpos=p, gamma=3, R=p,
+                ell=1, ghat=p, gsum=None, sqerr=None, ws=p, ws_bytes=ws, stream=None)
+
+    def direct(**kw):
+        return lib.gc_decode_direct(*{**args, **kw}.values())
+    assert direct(ell=0) == E and direct(ell=9) == E and direct(g_dtype=3) == E
+    assert direct(ghat=None) == E                                       # neither output
+    assert direct(sqerr=p) == E                                         # sqerr without gsum
+    assert direct(ws_bytes=ws - 1) == E and direct(ws=None) == E        # workspace
+    assert direct(ws=p + 4) == E                                        # unaligned workspace
+    assert direct(holder=None) == E and direct(G=None) == E
+    assert direct(P=0) == gcx.GC_OK
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 5, p, p, 1 << 20, None) == E                # loss
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 0, p, p, 4, None) == E                      # small ws
     assert lib.gc_sum_chunks(p, 3, 2, 8, p, None) == E
@@ -121,6 +134,11 @@ def test_workspace_sizes():
     assert gcx.gc_reconstruct_workspace_size(10, 50, 1024, 1) == 0
     assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 4) == 0
     assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 128
+    # direct estimate: fp32 mixing rows padded to 32 columns (256-byte rounded), then one fp64
+    # error partial per (row, 128-column tile)
+    assert gcx.gc_decode_direct_workspace_size(10000, 50, 16384, 1) == 4 * 10000 * 64 + 8 * 10000 * 128
+    assert gcx.gc_decode_direct_workspace_size(3, 6, 64, 3) == 1280 + 8 * 9  # 4*9*32 = 1152 -> 1280
+    assert gcx.gc_decode_direct_workspace_size(0, 6, 64, 1) == 0
 
 
 def test_assign_regular_algorithm2():
