@@ -218,7 +218,10 @@ int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P
  * G [N][d] (g_dtype GC_F32 or GC_BF16 bits), psi [P][m], holder/hpos
  * [N][gamma] (gc_assign), R [ell][m]: device.  Outputs as in gc_reconstruct:
  * ghat [P][d] fp32 (may be NULL), and with gsum [d] non-NULL, sqerr [P] fp64
- * (may be NULL; deterministic).  At least one of ghat, sqerr.  workspace:
+ * (may be NULL; deterministic), where each difference ghat - gsum, its square
+ * and the sum of four neighbouring squares are formed in fp32 and every further
+ * sum in fp64, so sqerr[p] is within a relative 6 * 2^-24 of the squared error
+ * of the returned ghat.  At least one of ghat, sqerr.  workspace:
  * device, 16-byte aligned, at least gc_decode_direct_workspace_size(P, N, d,
  * ell) bytes.  Rows of psi must be valid (0 <= psi[p][j] <= load of j).
  * Requires N, m <= GC_MAX_M.

@@ -26,6 +26,19 @@ inline int check_device() {
   return ok ? GC_OK : GC_ENOTSUP;
 }
 
+// Compute units of the current device (cached per device); 256 on MI355X.
+inline int cu_count() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (dev >= 0 && dev < 64 && cached[dev]) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+    n = 256;
+  if (dev >= 0 && dev < 64) cached[dev] = n;
+  return n;
+}
+
 inline int launch_status() {
   return hipGetLastError() == hipSuccess ? GC_OK : GC_ELAUNCH;
 }

@@ -14,12 +14,18 @@
 //   mix_kernel      one wavefront per pattern, one lane per chunk: coverage and
 //                   the ell x ell mixing block in fp64 (Cholesky of X^T X),
 //                   rounded once to fp32 into C (row stride padded to Kp).
-//   direct_kernel   128 x 128-tiled v_mfma_f32_32x32x2f32 GEMM of C and the
-//                   block-split gradients; A tiles [row][k] in LDS, B tiles
-//                   [k][col]; the estimate written with column guards.
-//                   With a target it also sums each row's squared error over the
-//                   tile's columns into per-(row, tile) fp64 partials.
+//   direct_short_kernel  K = N*ell <= 64: persistent blocks walk 128 x 128 output
+//                   tiles with the mixing rows resident in LDS and the next gradient
+//                   tile prefetched into registers.
+//   direct_kernel   any K: one 128 x 128 tile per block, k staged through
+//                   double-buffered LDS.
+//   Both run v_mfma_f32_32x32x2f32 with the gradients as first operand, so each
+//   lane ends with runs of four positions of one estimate row: 16-byte stores,
+//   and with a target the row's squared error over the tile (per-(row, tile)
+//   fp64 partials) needs one cross-lane exchange.
 //   direct_sqerr_kernel  adds the partials of each pattern in a fixed order.
+#include <algorithm>
+
 #include "common.h"
 
 namespace gcx {
@@ -150,25 +156,133 @@ __device__ __forceinline__ float gval<float>(const float *p) { return *p; }
 template <>
 __device__ __forceinline__ float gval<uint16_t>(const uint16_t *p) { return bf16_to_f32(*p); }
 
-// ghat[p*d + k*L + x] = sum_c C[(p*ell + k)*Kp + c] * G_blk[c][x],
-// G_blk[i*ell + k'][x] = g_i[k'*L + x] (zero past d).  With part != NULL the block also
-// writes part[r*ntiles + nt] = sum over its columns of (ghat[r][x] - gsum[k*L + x])^2 (fp64).
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Four gradient entries G_blk[c][x .. x+3], G_blk[i*ell + k'][x] = g_i[k'*L + x], zero past
+// the block (x >= L) or the gradient (k'*L + x >= d) and for c >= K.
+template <typename GT, bool VEC4, int ELL>
+__device__ __forceinline__ float4 gload4(const GT *__restrict__ G, int K, int64_t d, int64_t L,
+                                         int c, int64_t x) {
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (c < K) {
+    const int i = c / ELL, kk = c % ELL;
+    const int64_t col = kk * L + x;
+    const GT *src = G + int64_t(i) * d + col;
+    if (VEC4) {  // d and L multiples of 4, G aligned: all four in or all four out
+      if (x < L && col < d) {
+        if constexpr (sizeof(GT) == 4) {
+          const float4 f = *reinterpret_cast<const float4 *>(src);
+          v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+        } else {
+          const uint2 u = *reinterpret_cast<const uint2 *>(src);
+          v[0] = __uint_as_float(u.x << 16); v[1] = __uint_as_float(u.x & 0xffff0000u);
+          v[2] = __uint_as_float(u.y << 16); v[3] = __uint_as_float(u.y & 0xffff0000u);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (x + e < L && col + e < d) v[e] = gval<GT>(src + e);
+    }
+  }
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+
+// The MFMAs take the gradient tile as their first operand and the mixing rows as their
+// second, so they produce the transposed tile: lane (h, li) of acc[xb][rb] holds estimate
+// row rb*32 + li (of the wave's 64 rows) at positions xb*32 + 8*(v/4) + 4h + v%4 (of the
+// wave's 64 columns).  Each lane thus owns runs of four consecutive positions of one row:
+// the estimate leaves as 16-byte stores, and a row's squared error over the wave's columns
+// is a sum inside the lane plus one exchange between the lane halves.
+//
+// Writes the tile's estimate (if ghat) and, if red2, red2[wn][row] = squared error of the
+// row over the wave's 64 columns: each difference, square and sum of four neighbours in
+// fp32, the rest in fp64, in a fixed order.  gs = target tile [ELL][kDN] in LDS.
+template <int ELL>
+__device__ __forceinline__ void direct_epilogue(const v16f (&acc)[2][2], int64_t mt, int64_t nt,
+                                                int64_t rows, int64_t d, int64_t L, bool vst,
+                                                float *__restrict__ ghat, const float *gs,
+                                                double (*red2)[kDM], int wm, int wn, int h,
+                                                int li) {
+  const int64_t p0 = mt * kDM / ELL;  // pattern and block of the tile's first row
+  const int k0 = int(mt * kDM % ELL);
+  const bool tail = (ELL - 1) * L + (nt + 1) * kDN > d;  // the tile reaches past d somewhere
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    const int rl = wm * 64 + rb * 32 + li;
+    const int64_t r = mt * kDM + rl;
+    const int64_t p = p0 + (k0 + rl) / ELL;
+    const int k = (k0 + rl) % ELL;
+    double rs = 0.0;
+#pragma unroll
+    for (int xb = 0; xb < 2; ++xb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int xl = wn * 64 + xb * 32 + 8 * g + 4 * h;
+        const float e0 = acc[xb][rb][4 * g], e1 = acc[xb][rb][4 * g + 1];
+        const float e2 = acc[xb][rb][4 * g + 2], e3 = acc[xb][rb][4 * g + 3];
+        if (ghat && r < rows) {
+          const int64_t x = nt * kDN + xl;
+          const int64_t col = k * L + x;
+          float *dst = ghat + p * d + col;
+          // plain stores: a wave completes each 128-byte line of a row in eight 16-byte
+          // pieces, which the L2 merges before writing back
+          if (vst) {
+            if (x < L && col < d) *reinterpret_cast<v4f *>(dst) = v4f{e0, e1, e2, e3};
+          } else {
+            const float ev[4] = {e0, e1, e2, e3};
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (x + u < L && col + u < d) dst[u] = ev[u];
+          }
+        }
+        if (red2) {
+          // past the block (x >= L) both sides hold zero; the zero-padded tail of the last
+          // block (k*L + x >= d) is not part of the estimate and is masked out
+          const float4 t4 = *reinterpret_cast<const float4 *>(gs + k * kDN + xl);
+          float d0 = e0 - t4.x, d1 = e1 - t4.y, d2 = e2 - t4.z, d3 = e3 - t4.w;
+          if (tail) {
+            const int64_t col = k * L + nt * kDN + xl;
+            d0 = col < d ? d0 : 0.f;
+            d1 = col + 1 < d ? d1 : 0.f;
+            d2 = col + 2 < d ? d2 : 0.f;
+            d3 = col + 3 < d ? d3 : 0.f;
+          }
+          rs += double((d0 * d0 + d1 * d1) + (d2 * d2 + d3 * d3));
+        }
+      }
+    if (red2) {
+      const double o = __shfl_xor(rs, 32, kWave);
+      if (h == 0) red2[wn][rl] = rs + o;
+    }
+  }
+}
+
+// Fills the target tile gs[k][x] = gsum[k*L + nt*kDN + x] (zero past the block or d).
+template <int ELL>
+__device__ __forceinline__ void load_target(const float *__restrict__ gsum, int64_t nt, int64_t d,
+                                            int64_t L, float *gs, int t) {
+  for (int e = t; e < ELL * kDN; e += kDThreads) {
+    const int k = e / kDN;
+    const int64_t x = nt * kDN + e % kDN, col = k * L + x;
+    gs[e] = (x < L && col < d) ? gsum[col] : 0.f;
+  }
+}
+
+// ghat[p*d + k*L + x] = sum_c C[(p*ell + k)*Kp + c] * G_blk[c][x] for any K, in k stages of
+// kDK through double-buffered LDS; one 128 x 128 tile per block.  With part != NULL it also
+// writes part[r*ntiles + nt] = the row's squared error over the tile's columns.
 constexpr int kDLdsA = 2 * kDM * (kDK + kDPad), kDLdsB = 2 * kDK * (kDN + 4);
-constexpr int kDRedStride = 2 * 32 + 1;  // doubles per row of the error reduction
-static_assert((kDLdsA + kDLdsB) * 4 >= kDM * kDRedStride * 8, "reduction fits the tile buffers");
 
 template <typename GT, bool VEC4, int ELL>
-__global__ __launch_bounds__(kDThreads, 2) void direct_kernel(const float *__restrict__ C,
-                                                               const GT *__restrict__ G, int N,
-                                                               int64_t d, int64_t L,
-                                                               int64_t Kp, int64_t rows,
-                                                               int64_t ntiles,
-                                                               float *__restrict__ ghat,
-                                                               const float *__restrict__ gsum,
-                                                               double *__restrict__ part) {
-  __shared__ __align__(16) float smem[kDLdsA + kDLdsB];
-  auto As = reinterpret_cast<float(*)[kDM][kDK + kDPad]>(smem);
-  auto Bs = reinterpret_cast<float(*)[kDK][kDN + 4]>(smem + kDLdsA);
+__global__ __launch_bounds__(kDThreads, 2) void direct_kernel(
+    const float *__restrict__ C, const GT *__restrict__ G, int N, int64_t d, int64_t L, int64_t Kp,
+    int64_t rows, int64_t ntiles, bool vst, float *__restrict__ ghat,
+    const float *__restrict__ gsum, double *__restrict__ part) {
+  __shared__ __align__(16) float As[2][kDM][kDK + kDPad];
+  __shared__ __align__(16) float Bs[2][kDK][kDN + 4];
+  __shared__ __align__(16) float gs[ELL * kDN];
+  __shared__ double red2[2][kDM];
   // consecutive blocks take the column tiles of one row tile of C
   const int64_t nt = blockIdx.x % ntiles;
   const int64_t mt = blockIdx.x / ntiles;
@@ -185,29 +299,7 @@ __global__ __launch_bounds__(kDThreads, 2) void direct_kernel(const float *__res
       const int64_t r = mt * kDM + arow + 32 * p4;
       ra[p4] = r < rows ? *reinterpret_cast<const float4 *>(C + r * Kp + kb + ak)
                         : make_float4(0.f, 0.f, 0.f, 0.f);
-      const int c = int(kb) + brow + 8 * p4;  // (chunk, block) index
-      const int64_t x = nt * kDN + bc;
-      float v[4] = {0.f, 0.f, 0.f, 0.f};
-      if (c < K) {
-        const int i = c / ELL, kk = c % ELL;
-        const int64_t col = kk * L + x;
-        const GT *src = G + int64_t(i) * d + col;
-        if (VEC4 && x + 3 < L && col + 3 < d) {
-          if constexpr (sizeof(GT) == 4) {
-            const float4 f = *reinterpret_cast<const float4 *>(src);
-            v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-          } else {
-            const uint2 u = *reinterpret_cast<const uint2 *>(src);
-            v[0] = __uint_as_float(u.x << 16); v[1] = __uint_as_float(u.x & 0xffff0000u);
-            v[2] = __uint_as_float(u.y << 16); v[3] = __uint_as_float(u.y & 0xffff0000u);
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (x + e < L && col + e < d) v[e] = gval<GT>(src + e);
-        }
-      }
-      rb[p4] = make_float4(v[0], v[1], v[2], v[3]);
+      rb[p4] = gload4<GT, VEC4, ELL>(G, K, d, L, int(kb) + brow + 8 * p4, nt * kDN + bc);
     }
   };
   auto lstore = [&](int buf) {
@@ -226,6 +318,7 @@ __global__ __launch_bounds__(kDThreads, 2) void direct_kernel(const float *__res
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
 
+  if (part) load_target<ELL>(gsum, nt, d, L, gs, t);
   const int64_t nst = Kp / kDK;
   gload(0);
   lstore(0);
@@ -239,20 +332,20 @@ __global__ __launch_bounds__(kDThreads, 2) void direct_kernel(const float *__res
     for (int s4 = 0; s4 < 4; ++s4) {
       float4 a[2];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-        a[mb] = *reinterpret_cast<const float4 *>(&As[buf][wm * 64 + mb * 32 + li][h * 16 + s4 * 4]);
+      for (int rbk = 0; rbk < 2; ++rbk)
+        a[rbk] = *reinterpret_cast<const float4 *>(&As[buf][wm * 64 + rbk * 32 + li][h * 16 + s4 * 4]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int kk = h * 16 + s4 * 4 + e;
         float bv[2];
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) bv[nb] = Bs[buf][kk][wn * 64 + nb * 32 + li];
+        for (int xb = 0; xb < 2; ++xb) bv[xb] = Bs[buf][kk][wn * 64 + xb * 32 + li];
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-          const float av = e == 0 ? a[mb].x : (e == 1 ? a[mb].y : (e == 2 ? a[mb].z : a[mb].w));
+        for (int rbk = 0; rbk < 2; ++rbk) {
+          const float av = e == 0 ? a[rbk].x : (e == 1 ? a[rbk].y : (e == 2 ? a[rbk].z : a[rbk].w));
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv[nb], acc[mb][nb], 0, 0, 0);
+          for (int xb = 0; xb < 2; ++xb)
+            acc[xb][rbk] = __builtin_amdgcn_mfma_f32_32x32x2f32(bv[xb], av, acc[xb][rbk], 0, 0, 0);
         }
       }
     }
@@ -260,46 +353,126 @@ __global__ __launch_bounds__(kDThreads, 2) void direct_kernel(const float *__res
     __syncthreads();
   }
 
-  // lane (h, li) of wave (wm, wn) holds rows wm*64 + mb*32 + 8*(v/4) + 4h + v%4, columns
-  // wn*64 + nb*32 + li of the tile
-  double *red = reinterpret_cast<double *>(smem);  // [kDM][kDRedStride], free after the loop
-  const int64_t p0 = mt * kDM / ELL;                // pattern and block of the tile's first row
-  const int k0 = int(mt * kDM % ELL);
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int rl = wm * 64 + mb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-      const int64_t r = mt * kDM + rl;
-      const int64_t p = p0 + (k0 + rl) / ELL;
-      const int k = (k0 + rl) % ELL;
-      double e2 = 0.0;
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        const int64_t x = nt * kDN + wn * 64 + nb * 32 + li;
-        const int64_t col = k * L + x;
-        if (r < rows && x < L && col < d) {
-          const float g = acc[mb][nb][v];
-          if (ghat) __builtin_nontemporal_store(g, ghat + p * d + col);
-          if (part) {
-            const double e = double(g) - double(gsum[col]);
-            e2 += e * e;
-          }
-        }
-      }
-      if (part) red[rl * kDRedStride + wn * 32 + li] = e2;
-    }
+  direct_epilogue<ELL>(acc, mt, nt, rows, d, L, vst, ghat, gs, part ? red2 : nullptr, wm, wn, h, li);
   if (part) {
     __syncthreads();
-    // two threads per row, 32 entries each, then the pair is added: a fixed order
-    const int rl = t >> 1;
-    const double *src = red + rl * kDRedStride + (t & 1) * 32;
-    double s = 0.0;
-#pragma unroll 8
-    for (int c = 0; c < 32; ++c) s += src[c];
-    s += __shfl_xor(s, 1, kWave);
-    const int64_t r = mt * kDM + rl;
-    if ((t & 1) == 0 && r < rows) part[r * ntiles + nt] = s;
+    const int64_t r = mt * kDM + t;
+    if (t < kDM && r < rows) part[r * ntiles + nt] = red2[0][t] + red2[1][t];
+  }
+}
+
+// Short contractions (K = N*ell <= 64, padded to Kq, a multiple of 4): a persistent grid walks
+// the (row tile, column tile) pairs in row-tile-major order, each block a contiguous range.
+// The block's A rows (128 x Kq) stay in LDS while its row tile does not change; the next
+// column tile of the gradients is loaded into registers while the current one is
+// multiplied.  Lane half h takes k in [h*Kh, (h+1)*Kh), Kh = Kq/2, from LDS layouts whose
+// two halves sit 32 banks apart, so the 64 lanes of a read hit 64 distinct banks.
+constexpr int kSKMax = 64;                           // largest Kq of the short path
+constexpr int kSAStride = 33;                        // words per A row of one half (odd)
+constexpr int kSAHalf = kDM * kSAStride + 32;        // A half 1 starts 32 banks after half 0
+constexpr int kSBHalf = (kSKMax / 2) * kDN + 32;     // likewise for B
+constexpr int kSLds = 2 * kSAHalf + 2 * kSBHalf + GC_MAX_ELL * kDN;  // floats; + red2 below
+
+template <typename GT, bool VEC4, int ELL>
+__global__ __launch_bounds__(kDThreads, 2) void direct_short_kernel(
+    const float *__restrict__ C, const GT *__restrict__ G, int N, int64_t d, int64_t L, int64_t Kp,
+    int Kq, int64_t rows, int64_t ntiles, int64_t ntotal, bool vst, float *__restrict__ ghat,
+    const float *__restrict__ gsum, double *__restrict__ part) {
+  __shared__ __align__(16) float smem[kSLds];
+  __shared__ double red2[2][kDM];
+  float *As = smem;                  // [2][kDM][kSAStride] (+ gap)
+  float *Bs = smem + 2 * kSAHalf;    // [2][Kh][kDN] (+ gap)
+  float *gs = Bs + 2 * kSBHalf;      // [ELL][kDN]
+  const int t = threadIdx.x, lane = t % kWave, wave = t / kWave;
+  const int wm = wave >> 1, wn = wave & 1, h = lane >> 5, li = lane & 31;
+  const int K = N * ELL, Kh = Kq >> 1;
+  const int64_t q0 = int64_t(blockIdx.x) * ntotal / gridDim.x;
+  const int64_t q1 = int64_t(blockIdx.x + 1) * ntotal / gridDim.x;
+
+  // B rows c = (t >> 5) + 8j, columns 4*(t & 31) .. +3; target entries t + 256j
+  constexpr int kTgt = (ELL * kDN + kDThreads - 1) / kDThreads;
+  float4 rb[kSKMax / 8];
+  float rg[kTgt];
+  auto prefetch = [&](int64_t q) {
+    const int64_t nt = q % ntiles;
+    const int64_t x = nt * kDN + (t & 31) * 4;
+#pragma unroll
+    for (int j = 0; j < kSKMax / 8; ++j) rb[j] = gload4<GT, VEC4, ELL>(G, K, d, L, (t >> 5) + 8 * j, x);
+    if (part) {
+#pragma unroll
+      for (int j = 0; j < kTgt; ++j) {
+        const int e = t + j * kDThreads, k = e / kDN;
+        const int64_t xx = nt * kDN + e % kDN, col = k * L + xx;
+        rg[j] = (e < ELL * kDN && xx < L && col < d) ? gsum[col] : 0.f;
+      }
+    }
+  };
+  auto commit = [&]() {
+#pragma unroll
+    for (int j = 0; j < kSKMax / 8; ++j) {
+      const int c = (t >> 5) + 8 * j;
+      if (c < Kq) {
+        const int hh = c >= Kh ? 1 : 0;
+        *reinterpret_cast<float4 *>(Bs + hh * kSBHalf + (c - hh * Kh) * kDN + (t & 31) * 4) = rb[j];
+      }
+    }
+    if (part) {
+#pragma unroll
+      for (int j = 0; j < kTgt; ++j)
+        if (t + j * kDThreads < ELL * kDN) gs[t + j * kDThreads] = rg[j];
+    }
+  };
+
+  int64_t cur_mt = -1;
+  if (q0 < q1) prefetch(q0);
+  for (int64_t q = q0; q < q1; ++q) {
+    const int64_t mt = q / ntiles, nt = q % ntiles;
+    if (mt != cur_mt) {
+      // A rows of the new row tile: C[(mt*128 + r)][0 .. Kq), zero past the last row
+      for (int e = t; e < kDM * (Kq >> 2); e += kDThreads) {
+        const int r = e / (Kq >> 2), c = (e % (Kq >> 2)) * 4;
+        const int64_t gr = mt * kDM + r;
+        const float4 a = gr < rows ? *reinterpret_cast<const float4 *>(C + gr * Kp + c)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float av[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int cc = c + u, hh = cc >= Kh ? 1 : 0;
+          As[hh * kSAHalf + r * kSAStride + (cc - hh * Kh)] = av[u];
+        }
+      }
+      cur_mt = mt;
+    }
+    commit();
+    __syncthreads();
+    if (q + 1 < q1) prefetch(q + 1);
+
+    v16f acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
+    const float *Ah = As + h * kSAHalf + (wm * 64 + li) * kSAStride;
+    const float *Bh = Bs + h * kSBHalf + wn * 64 + li;
+#pragma unroll 2
+    for (int ks = 0; ks < Kh; ++ks) {
+      const float a0 = Ah[ks], a1 = Ah[32 * kSAStride + ks];
+      const float b0 = Bh[ks * kDN], b1 = Bh[ks * kDN + 32];
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(b0, a0, acc[0][0], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a0, acc[1][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b0, a1, acc[0][1], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a1, acc[1][1], 0, 0, 0);
+    }
+
+    direct_epilogue<ELL>(acc, mt, nt, rows, d, L, vst, ghat, gs, part ? red2 : nullptr, wm, wn, h,
+                         li);
+    __syncthreads();
+    if (part && t < kDM) {
+      const int64_t r = mt * kDM + t;
+      if (r < rows) part[r * ntiles + nt] = red2[0][t] + red2[1][t];
+    }
   }
 }
 
@@ -380,11 +553,21 @@ extern "C" int gc_decode_direct(const void *G, int32_t g_dtype, int32_t N, int64
   }
   const size_t es = g_dtype == GC_F32 ? 4 : 2;
   const bool vec4 = d % 4 == 0 && L % 4 == 0 && (reinterpret_cast<uintptr_t>(G) % (4 * es)) == 0;
+  const bool vst = d % 4 == 0 && L % 4 == 0 && (reinterpret_cast<uintptr_t>(ghat) % 16) == 0;
   const dim3 grid{static_cast<uint32_t>(blocks)};
   const bool f32 = g_dtype == GC_F32;
+  const int Kq = int(ceil_div(int64_t(N) * ell, 4) * 4);
+  const int64_t ntotal = ceil_div(rows, kDM) * ntiles;
+  const bool short_k = Kq <= kSKMax;
+  const dim3 sgrid{static_cast<uint32_t>(std::min<int64_t>(ntotal, 2 * int64_t(cu_count())))};
 #define GC_DIRECT(GT, V, E)                                                                        \
-  hipLaunchKernelGGL((direct_kernel<GT, V, E>), grid, dim3(kDThreads), 0, stream, Cm,              \
-                     static_cast<const GT *>(G), N, d, L, Kp, rows, ntiles, ghat, gsum, part)
+  if (short_k)                                                                                     \
+    hipLaunchKernelGGL((direct_short_kernel<GT, V, E>), sgrid, dim3(kDThreads), 0, stream, Cm,     \
+                       static_cast<const GT *>(G), N, d, L, Kp, Kq, rows, ntiles, ntotal, vst,     \
+                       ghat, gsum, part);                                                          \
+  else                                                                                             \
+    hipLaunchKernelGGL((direct_kernel<GT, V, E>), grid, dim3(kDThreads), 0, stream, Cm,            \
+                       static_cast<const GT *>(G), N, d, L, Kp, rows, ntiles, vst, ghat, gsum, part)
 #define GC_DIRECT_ELL(E)                                                                           \
   case E:                                                                                          \
     if (f32) {                                                                                     \

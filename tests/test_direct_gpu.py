@@ -66,7 +66,7 @@ def test_direct_tiny_every_pattern(ell):
     G64 = R_.chunk_grads(X, y, w, wl.loss)
     G = G64.astype(np.float32)
     psi = gen.psi(wl)
-    O, R, ghat, sqerr, _ = run_direct(wl, G, psi, ell)
+    O, R, ghat, sqerr, gsum = run_direct(wl, G, psi, ell)
     ref, _ = check_elementwise(O, psi, R, G.astype(np.float64), host(ghat).astype(np.float64), "tiny")
     # the same estimate through the protocol's own route (Algorithm 1 at every worker)
     e2e = R_.end_to_end(O, psi, R, G.astype(np.float64), per_worker=True)
@@ -74,6 +74,8 @@ def test_direct_tiny_every_pattern(ell):
     tgt = G.astype(np.float64).sum(axis=0)
     se_ref = ((ref - tgt) ** 2).sum(axis=1)
     se = host(sqerr)
+    se_gh = ((host(ghat).astype(np.float64) - host(gsum).astype(np.float64)) ** 2).sum(axis=1)
+    assert (np.abs(se - se_gh) <= 8 * R_.U * se_gh + 1e-30).all()
     scale = float((np.abs(G.astype(np.float64)).sum(axis=0) ** 2).sum())
     assert (np.abs(se - se_ref) <= 1e-5 * scale).all()
     # at ell = 1 the 100 patterns hold both decodable and non-decodable ones
@@ -110,9 +112,18 @@ def test_direct_ragged(N, d, ell, dtype):
     psi = gen.psi(wl)
     psi[::10] = wl.delta                     # every tenth pattern: no stragglers (exact)
     G64 = OP.widen(G, dtype)
-    O, R, ghat, sqerr, _ = run_direct(wl, G, psi, ell, dtype)
+    O, R, ghat, sqerr, gsum = run_direct(wl, G, psi, ell, dtype)
     gh = host(ghat).astype(np.float64)
-    check_elementwise(O, psi, R, G64, gh, wl.name)
+    ref, _ = check_elementwise(O, psi, R, G64, gh, wl.name)
+    # squared errors: those of the returned estimate (fp32 differences and squares: relative
+    # 6 * 2^-24), and the oracle's up to the estimate's own error
+    se = host(sqerr)
+    tgt32 = host(gsum).astype(np.float64)
+    se_gh = ((gh - tgt32) ** 2).sum(axis=1)
+    assert (np.abs(se - se_gh) <= 8 * R_.U * se_gh + 1e-30).all()
+    se_ref = ((ref - G64.sum(axis=0)) ** 2).sum(axis=1)
+    scale = float((np.abs(G64).sum(axis=0) ** 2).sum())
+    assert (np.abs(se - se_ref) <= 1e-5 * scale).all()
     # error-only mode gives the same squared errors, bit for bit
     _, _, g2, se2, _ = run_direct(wl, G, psi, ell, dtype, want_ghat=False)
     assert g2 is None and np.array_equal(host(se2), host(sqerr))
