@@ -21,7 +21,7 @@
 namespace gcx {
 namespace {
 
-constexpr int kEncThreads = 512;
+constexpr int kEncThreads = 1024;
 constexpr int kEncWaves = kEncThreads / kWave;
 constexpr size_t kEncSliceLds = 96 * 1024;   // G slice budget
 constexpr size_t kEncMetaLds = 24 * 1024;    // row metadata budget
@@ -209,8 +209,14 @@ int launch_encode(EncodeArgs a, hipStream_t st) {
   if (group > kEncMaxGroup) group = kEncMaxGroup;
   if (group < 1) group = 1;
   a.group_rows = group;
-  a.rows_per_block = kEncRowsPerBlock;
-  const int64_t rblocks = ceil_div(a.rows, a.rows_per_block);
+  // at most kEncRowsPerBlock rows per block, and a grid that is a whole number of rounds of
+  // the blocks the chip holds at once (two per CU), so no round runs partly empty
+  const int64_t conc = 2 * int64_t(cu_count());
+  int64_t g = a.nslices, h = conc;
+  while (h) { const int64_t t = g % h; g = h; h = t; }
+  const int64_t step = conc / g;  // row blocks per round of the grid
+  const int64_t rblocks = ceil_div(ceil_div(a.rows, kEncRowsPerBlock), step) * step;
+  a.rows_per_block = ceil_div(a.rows, rblocks);
   const int64_t blocks = rblocks * a.nslices;
   if (!grid_ok(blocks, kEncThreads)) return GC_EINVAL;
   const size_t lds = gbytes + per_row * group;
