@@ -173,3 +173,72 @@ def test_direct_headline_full_size(headline_G, ell):
         se = se[pats]
     scale = np.linalg.norm(tgt)
     assert (np.abs(np.sqrt(se) - np.sqrt(se_ref)) <= 1e-5 * scale + 1e-4 * np.sqrt(se_ref)).all()
+
+
+def check_sampled_direct(O, psi, R, G, dtype, ghat_d, pats, xs):
+    """The estimate at positions k*L + xs of patterns pats against the oracle's
+    sum_i M_i g_i computed on just those positions (``oracle_runs.sampled_blocks``)."""
+    ell = R.shape[0]
+    d = G.shape[1]
+    L = -(-d // ell)
+    Gsub = R_.sampled_blocks(G, dtype, ell, xs)                 # blocks of width len(xs)
+    cols = [k * L + int(x) for k in range(ell) for x in xs]
+    keep = [a for a, c in enumerate(cols) if c < d]
+    idx = torch.as_tensor([cols[a] for a in keep], device="cuda")
+    ref, mag, kap = R_.direct_ref(O, psi[pats], R, Gsub)         # [len(pats)][ell*len(xs)]
+    magG = np.tile(np.abs(R_.gblocks(Gsub, ell)).sum(axis=(0, 1)), ell)
+    K = O.shape[0] * ell
+    for a, p in enumerate(pats):
+        gh = host(ghat_d[p][idx]).astype(np.float64)
+        bound = 2 * R_.gamma(K + 2) * mag[a][keep] + 1e-13 * kap[a] ** 2 * magG[keep]
+        assert (np.abs(gh - ref[a][keep]) <= bound + 1e-30).all(), (p, np.abs(gh - ref[a][keep]).max())
+
+
+def test_direct_bandwidth_full_size():
+    """m = 100, d = 2^20, fp32 gradients: 12 patterns at ell = 1, 2, 8 (K up to 800 through the
+    k-staged kernel, 8,192 column tiles at ell = 1), sampled positions against the oracle."""
+    from workloads import BANDWIDTH
+    wl = BANDWIDTH
+    O, order, holder, hpos = tables(wl)
+    psi = gen.psi(wl, count=12)
+    psi[5] = 0                                   # nothing processed: estimate zero
+    G = gen.given_G(wl, threads=16)
+    Gd = dev(G)
+    gsum = gcx.gc_sum_chunks(Gd)
+    for ell in (1, 2, 8):
+        R = gen.shared_R(wl.m, ell)
+        ghat, sqerr = gcx.gc_decode_direct(Gd, dev(psi), dev(order), dev(holder), dev(hpos), dev(R),
+                                           gsum=gsum)
+        L = -(-wl.d // ell)
+        xs = np.sort(np.random.default_rng(30 + ell).choice(L, 48, replace=False))
+        check_sampled_direct(O, psi, R, G, "f32", ghat, [0, 3, 5, 11], xs)
+        assert float(host(ghat[5]).__abs__().max()) == 0.0
+        tgt = host(gsum).astype(np.float64)
+        assert abs(host(sqerr)[5] - (tgt ** 2).sum()) <= 1e-5 * (tgt ** 2).sum()
+        del ghat
+        torch.cuda.empty_cache()
+
+
+def test_direct_large_bf16_full_length():
+    """m = 200, d = 2^24, bf16 gradients, least-squares patterns (50% forced stragglers):
+    two patterns at full length for ell = 1, 2, 4, sampled positions against the oracle."""
+    from workloads import LARGE
+    wl = LARGE
+    O, order, holder, hpos = tables(wl)
+    psi = gen.psi(wl, count=2, variant="ls")
+    G = gen.given_G(wl, threads=16)
+    Gd = dev(G.view(np.int16)).view(torch.bfloat16)
+    gsum = gcx.gc_sum_chunks(Gd)
+    for ell in (1, 2, 4):
+        R = gen.shared_R(wl.m, ell)
+        ghat, sqerr = gcx.gc_decode_direct(Gd, dev(psi), dev(order), dev(holder), dev(hpos), dev(R),
+                                           gsum=gsum)
+        L = -(-wl.d // ell)
+        xs = np.sort(np.random.default_rng(40 + ell).choice(L, 24, replace=False))
+        check_sampled_direct(O, psi, R, G, "bf16", ghat, [0, 1], xs)
+        # the squared error agrees with the estimate it comes with
+        gh = host(ghat).astype(np.float64)
+        se_gh = ((gh - host(gsum).astype(np.float64)) ** 2).sum(axis=1)
+        assert (np.abs(host(sqerr) - se_gh) <= 8 * R_.U * se_gh).all()
+        del ghat, gh
+        torch.cuda.empty_cache()
