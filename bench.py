@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--mfma-points", type=int, default=256,
                     help="also time the chunk gradients at this many evaluation points (matrix-core "
                          "path; 0 = skip); reported under 'mfma', outside the step")
+    ap.add_argument("--no-decode-large", dest="decode_large", action="store_false",
+                    help="skip timing the coefficients of the 100,000-pattern m = 200 workload "
+                         "(reported under 'decode_large', outside the step)")
     ap.add_argument("--no-direct", dest="direct", action="store_false",
                     help="skip timing gc_decode_direct (reported under 'direct', outside the step)")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
@@ -64,7 +67,7 @@ def algorithmic_bytes(wl, ell, P, sent):
     enc = 4 * sent * L + 4 * N * d + 4 * P * m + 4 * P * m * delta * ell + 4 * m * delta
     rec = 4 * sent * L + 4 * P * m + 4 * P * d + 4 * ell * m + 4 * d + 8 * P
     dcd = 4 * P * m + 4 * P * N + P + 4 * P + 4 * P * m * delta * ell + 4 * ell * m + 12 * N * delta
-    grads = 4 * N * wl.n * wl.d + 4 * N * wl.n + 4 * d + 4 * N * d
+    grads = (4 * N * wl.n * wl.d + 4 * N * wl.n + 4 * d + 4 * N * d) if wl.n else 0
     return {"gc_encode": enc, "gc_reconstruct": rec, "gc_decode_coeffs": dcd, "gc_chunk_grads": grads,
             "gc_sum_chunks": 4 * N * d + 4 * d}
 
@@ -150,6 +153,45 @@ def time_direct(gcx, wl, ell, G, gsum, psid, orderd, holderd, hposd, Rd, ghat, s
             "flops": flops, "dtype": "f32", "ghat": True,
             "note": "gc_decode_direct: estimate of every pattern from the chunk gradients through "
                     "M_i = R[:, S_i] pinv(R[:, S_i]), outside the step"}
+
+
+def time_decode_large(gcx, reps=10):
+    """Coefficients for all 100,000 patterns of the m = 200, delta = 20 workload (exact run,
+    ell = 1): the decode's bandwidth point, 1.6 GB of Bc written per call."""
+    import torch
+    from workloads import LARGE, gen
+    wl = LARGE
+    psi = gen.psi(wl)
+    R = gen.shared_R(wl.m, 1)
+    _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, wl.N, wl.m, wl.s)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    psid, od, hd, hpd, Rd = d(psi), d(order), d(holder), d(hpos), d(R)
+    P = wl.P
+    cov = torch.empty((P, wl.N), dtype=torch.int32, device="cuda")
+    dec = torch.empty(P, dtype=torch.uint8, device="cuda")
+    cerr = torch.empty(P, dtype=torch.int32, device="cuda")
+    Bc = torch.empty((P, wl.m, wl.delta, 1), dtype=torch.float32, device="cuda")
+
+    def call():
+        gcx.gc_decode_coeffs(psid, od, hd, hpd, Rd, cov=cov, dec=dec, coef_err=cerr, Bc=Bc)
+    call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = algorithmic_bytes(wl, 1, P, 0)["gc_decode_coeffs"]
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out = {"workload": wl.name, "patterns": P, "ell": 1, "ms": ms, "patterns_per_s": P / (ms * 1e-3),
+           "bound": "hbm", "algorithmic_bytes": nbytes, "achieved": gbs, "peak": HBM_PEAK_GBS,
+           "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+           "decodable_frac": float((dec == 1).float().mean().item())}
+    del cov, dec, cerr, Bc
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(wl, ell, X, y, w, psi, R, budget_s):
@@ -399,6 +441,7 @@ def main():
         "kernels_ms": avg_ms,
         "kernels_gbs": gbs,
         "decoded_gradients_per_s": float((decs == 1).sum()) * args.steps / elapsed,
+        "coefficient_patterns_per_s": P / (avg_ms["gc_decode_coeffs"] * 1e-3),
         "quality": {"decodable_frac": float((decs == 1).mean()),
                     "mean_coef_err": float(cerr.float().mean().item()),
                     "mse_vs_sum_g": float(se.mean() / wl.d),
@@ -411,6 +454,10 @@ def main():
         out["direct"]["sqerr_max_abs_diff_vs_step"] = float(np.abs(np.sqrt(se_d) - np.sqrt(se)).max())
     if args.mfma_points > 0:
         out["mfma"] = time_many_points(gcx, wl, Xd, yd, args.mfma_points, dev)
+        if args.mfma_points != 64:
+            out["mfma_b64"] = time_many_points(gcx, wl, Xd, yd, 64, dev)
+    if args.decode_large:
+        out["decode_large"] = time_decode_large(gcx)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, ell, X, y, w, psi, R, args.cpu_seconds)
     print(json.dumps(out))

@@ -13,6 +13,8 @@
 // with a Cholesky factorisation of M or H.  ell = 1 reduces to Remark 1:
 // coefficient R_j / sum_{S_i} R^2.  Coverage and decodability are integer
 // decisions and never depend on the floating-point solve.
+#include <algorithm>
+
 #include "common.h"
 
 namespace gcx {
@@ -244,14 +246,304 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
   }
 }
 
+// Two-phase variant, used whenever the assignment tables fit in LDS.  A persistent block
+// stages the tables transposed ([gamma][N], so lane i's holder reads are consecutive
+// words) and each worker's load once; each wave then takes patterns in turn:
+//   phase 1, one lane per chunk: coverage, and the fp64 factor of the chunk's small
+//     system (ell = 1: sum_{S_i} R^2; Delta >= ell: Cholesky of X X^T; 0 < Delta < ell:
+//     Cholesky of the padded X^T X and the members), kept in the wave's LDS region;
+//   phase 2, one lane per coefficient row (j, t) in Bc order: the chunk order[j][t], and
+//     the coefficients recomputed from the stored factor with the same operations as the
+//     one-phase kernel, written contiguously.
+// Both phases read psi from the wave's LDS copy.  Results equal decode_kernel's, except
+// that at ell = 1 the coefficient R_j / sum R^2 is formed as R_j * (1 / sum R^2) in fp64
+// before the fp32 rounding.
 template <int ELL>
-void launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *order, int delta,
+struct DecodeLayout {
+  static constexpr int NF = ELL * (ELL + 1) / 2;  // packed lower triangle
+  // words (4 bytes) of the block-shared part and of one wave's region
+  __host__ __device__ static int64_t shared_words(int N, int m, int gamma) {
+    return (2 * int64_t(gamma) * N + m + int64_t(ELL) * m + 3) & ~int64_t(3);
+  }
+  __host__ __device__ static int64_t wave_words(int N, int m, bool bc) {
+    const int64_t f = bc ? 2 * int64_t(N) * NF : 0;        // doubles
+    const int64_t sel = (bc && ELL > 1) ? int64_t(N) * ELL : 0;
+    return (f + N + sel + m + 3) & ~int64_t(3);
+  }
+};
+
+// Blocks of up to 16 waves while the per-lane solve is small, 4 beyond (more registers).
+template <int ELL>
+constexpr int decode_tiled_max_waves() { return ELL <= 4 ? 16 : 4; }
+
+template <int ELL>
+__global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_tiled_kernel(
+    const int32_t *__restrict__ psi, int64_t P, int N, int m, const int32_t *__restrict__ order,
+    int delta, const int32_t *__restrict__ holder, const int32_t *__restrict__ hpos, int gamma,
+    const float *__restrict__ R, int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
+    int32_t *__restrict__ coef_err, float *__restrict__ Bc) {
+  using Lay = DecodeLayout<ELL>;
+  constexpr int NF = Lay::NF;
+  extern __shared__ __align__(16) int32_t sh[];
+  int32_t *holdT = sh;                           // [gamma][N]
+  int32_t *hposT = holdT + int64_t(gamma) * N;   // [gamma][N]
+  int32_t *loads = hposT + int64_t(gamma) * N;   // [m]
+  float *Rs = reinterpret_cast<float *>(loads + m);  // [ELL][m]
+  const bool want_bc = Bc != nullptr;
+  for (int e = threadIdx.x; e < N * gamma; e += blockDim.x) {
+    const int i = e / gamma, u = e % gamma;
+    holdT[int64_t(u) * N + i] = holder[e];
+    hposT[int64_t(u) * N + i] = hpos[e];
+  }
+  for (int j = threadIdx.x; j < m; j += blockDim.x) {
+    int load = 0;
+    for (int t = 0; t < delta; ++t) {
+      const int c = order[int64_t(j) * delta + t];
+      load += (c >= 0 && c < N) ? 1 : 0;
+    }
+    loads[j] = load;
+  }
+  if (want_bc)
+    for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
+  __syncthreads();  // the only block barrier; every thread reaches it
+
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  int32_t *region = sh + Lay::shared_words(N, m, gamma) + int64_t(wave) * Lay::wave_words(N, m, want_bc);
+  double *F = reinterpret_cast<double *>(region);                  // [N][NF]
+  int32_t *covS = region + (want_bc ? 2 * int64_t(N) * NF : 0);    // [N]
+  int32_t *sel = covS + N;                                          // [N][ELL] (ELL > 1)
+  int32_t *pss = sel + ((want_bc && ELL > 1) ? int64_t(N) * ELL : 0);  // [m]
+  const int64_t wstride = int64_t(delta) * ELL;
+
+  for (int64_t p = int64_t(blockIdx.x) * nw + wave; p < P; p += int64_t(gridDim.x) * nw) {
+    bool bad = false;
+    for (int j = lane; j < m; j += kWave) {
+      const int v = psi[p * m + j];
+      pss[j] = v;
+      bad = bad || v < 0 || v > loads[j];
+    }
+    const bool invalid = __any(bad);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // ---- phase 1: one lane per chunk
+    int err = 0;
+    bool all_ok = true;
+    for (int i = lane; i < N; i += kWave) {
+      int Delta = 0;
+      double ss = 0.0;  // ell = 1: sum of R_j^2 over the members, in holder order
+#pragma unroll 4
+      for (int u = 0; u < gamma; ++u) {
+        const int j = holdT[u * N + i], t = hposT[u * N + i];
+        if (j >= 0 && j < m && t >= 0 && t < delta && pss[j] > t) {
+          ++Delta;
+          if (ELL == 1 && want_bc) {
+            const double x = Rs[j];
+            ss += x * x;
+          }
+        }
+      }
+      if (cov != nullptr) cov[p * N + i] = Delta;
+      err += Delta < ELL ? ELL - Delta : 0;
+      all_ok = all_ok && Delta >= ELL;
+      covS[i] = Delta;
+      if (!want_bc) continue;
+      double *Fi = F + int64_t(i) * NF;
+      if constexpr (ELL == 1) {
+        // phase 2 multiplies by the reciprocal (one rounding more than a division); zero
+        // when nothing is covered or the pattern is invalid, so phase 2 writes zeros
+        Fi[0] = (invalid || Delta == 0) ? 0.0 : 1.0 / ss;
+        continue;
+      }
+      if (invalid || Delta == 0) continue;
+      if constexpr (ELL == 1) {
+      } else if (Delta >= ELL) {
+        double M[ELL][ELL];
+#pragma unroll
+        for (int a = 0; a < ELL; ++a)
+#pragma unroll
+          for (int b = 0; b < ELL; ++b) M[a][b] = 0.0;
+        for (int u = 0; u < gamma; ++u) {
+          const int j = holdT[u * N + i], t = hposT[u * N + i];
+          if (j >= 0 && j < m && t >= 0 && t < delta && pss[j] > t) {
+            double x[ELL];
+#pragma unroll
+            for (int k = 0; k < ELL; ++k) x[k] = Rs[k * m + j];
+#pragma unroll
+            for (int a = 0; a < ELL; ++a)
+#pragma unroll
+              for (int b = 0; b <= a; ++b) M[a][b] += x[a] * x[b];
+          }
+        }
+        cholesky<ELL>(M);
+#pragma unroll
+        for (int a = 0; a < ELL; ++a)
+#pragma unroll
+          for (int b = 0; b <= a; ++b) Fi[a * (a + 1) / 2 + b] = M[a][b];
+      } else {
+        int selj[ELL];
+#pragma unroll
+        for (int a = 0; a < ELL; ++a) selj[a] = -1;
+        int cnt = 0;
+        for (int u = 0; u < gamma; ++u) {
+          const int j = holdT[u * N + i], t = hposT[u * N + i];
+          if (j >= 0 && j < m && t >= 0 && t < delta && pss[j] > t) {
+#pragma unroll
+            for (int a = 0; a < ELL; ++a)
+              if (a == cnt) selj[a] = j;
+            ++cnt;
+          }
+        }
+        double X[ELL][ELL];
+#pragma unroll
+        for (int a = 0; a < ELL; ++a) {
+          const int ja = a < Delta ? selj[a] : 0;
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) X[k][a] = a < Delta ? double(Rs[k * m + ja]) : 0.0;
+        }
+        double H[ELL][ELL];
+#pragma unroll
+        for (int a = 0; a < ELL; ++a)
+#pragma unroll
+          for (int b = 0; b <= a; ++b) {
+            double v = 0.0;
+#pragma unroll
+            for (int k = 0; k < ELL; ++k) v += X[k][a] * X[k][b];
+            H[a][b] = (a < Delta) ? v : (a == b ? 1.0 : 0.0);
+          }
+        cholesky<ELL>(H);
+#pragma unroll
+        for (int a = 0; a < ELL; ++a) {
+          sel[int64_t(i) * ELL + a] = selj[a];
+#pragma unroll
+          for (int b = 0; b <= a; ++b) Fi[a * (a + 1) / 2 + b] = H[a][b];
+        }
+      }
+    }
+    err = wave_sum(err);
+    const bool ok = __all(all_ok);
+    if (lane == 0) {
+      dec[p] = invalid ? GC_DEC_INVALID : (ok ? GC_DEC_YES : GC_DEC_NO);
+      coef_err[p] = err;
+    }
+    if (!want_bc) continue;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // ---- phase 2: one lane per coefficient row (j, t), Bc order
+    float *Bp = Bc + p * int64_t(m) * wstride;
+#pragma unroll 4
+    for (int e = lane; e < m * delta; e += kWave) {
+      const int j = e / delta, t = e % delta;
+      const int c = order[e];
+      float out[ELL];
+#pragma unroll
+      for (int k = 0; k < ELL; ++k) out[k] = 0.f;
+      const bool valid = c >= 0 && c < N && pss[j] > t;
+      if constexpr (ELL == 1) {
+        if (valid && F[c] != 0.0) out[0] = float(double(Rs[j]) * F[c]);  // +0 otherwise
+      }
+      const int Delta = (ELL > 1 && valid) ? covS[c] : 0;
+      if (ELL > 1 && !invalid && Delta > 0) {
+        const double *Fc = F + int64_t(c) * NF;
+        if constexpr (ELL == 1) {
+        } else if (Delta >= ELL) {
+          double Lf[ELL][ELL];
+#pragma unroll
+          for (int a = 0; a < ELL; ++a)
+#pragma unroll
+            for (int b = 0; b < ELL; ++b) Lf[a][b] = b <= a ? Fc[a * (a + 1) / 2 + b] : 0.0;
+          double cc[ELL];
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) cc[k] = Rs[k * m + j];
+          chol_solve<ELL>(Lf, cc);
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) out[k] = float(cc[k]);
+        } else {
+          double Lf[ELL][ELL];
+#pragma unroll
+          for (int a = 0; a < ELL; ++a)
+#pragma unroll
+            for (int b = 0; b < ELL; ++b) Lf[a][b] = b <= a ? Fc[a * (a + 1) / 2 + b] : 0.0;
+          int selj[ELL];
+          int me = 0;  // j's place among the members
+#pragma unroll
+          for (int a = 0; a < ELL; ++a) {
+            selj[a] = sel[int64_t(c) * ELL + a];
+            if (a < Delta && selj[a] == j) me = a;
+          }
+          double X[ELL][ELL];
+#pragma unroll
+          for (int a = 0; a < ELL; ++a) {
+            const int ja = a < Delta ? selj[a] : 0;
+#pragma unroll
+            for (int k = 0; k < ELL; ++k) X[k][a] = a < Delta ? double(Rs[k * m + ja]) : 0.0;
+          }
+          double z[ELL];
+#pragma unroll
+          for (int b = 0; b < ELL; ++b) z[b] = (me == b) ? 1.0 : 0.0;
+          chol_solve<ELL>(Lf, z);
+#pragma unroll
+          for (int k = 0; k < ELL; ++k) {
+            double v = 0.0;
+#pragma unroll
+            for (int b = 0; b < ELL; ++b) v += z[b] * X[k][b];
+            out[k] = float(v);
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < ELL; ++k) Bp[int64_t(e) * ELL + k] = out[k];
+    }
+    // the next pattern overwrites this wave's region only after every lane is done with it
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+constexpr size_t kDecodeLdsCU = 160 * 1024;  // LDS of one CU
+
+template <int ELL>
+bool launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *order, int delta,
                    const int32_t *holder, const int32_t *hpos, int gamma, const float *R,
                    int32_t *cov, uint8_t *dec, int32_t *coef_err, float *Bc, hipStream_t st) {
+  using Lay = DecodeLayout<ELL>;
+  const bool bc = Bc != nullptr;
+  const size_t shared = 4 * size_t(Lay::shared_words(N, m, gamma));
+  const size_t per_wave = 4 * size_t(Lay::wave_words(N, m, bc));
+  // the most waves per CU the LDS allows (at most 32), in blocks of up to 16 waves
+  int best_w = 0, best_total = 0;
+  for (int w = decode_tiled_max_waves<ELL>(); w >= 1; w >>= 1) {
+    const size_t lds = shared + w * per_wave;
+    if (lds > kDecodeLdsCU) continue;
+    const int per_cu = int(std::min<size_t>(kDecodeLdsCU / lds, 32 / w));
+    if (per_cu * w > best_total) {
+      best_total = per_cu * w;
+      best_w = w;
+    }
+  }
+  if (best_total >= 8) {  // else the one-phase kernel, which needs no LDS per wave
+    const size_t lds = shared + best_w * per_wave;
+    const int64_t want = ceil_div(P, best_w);
+    const int64_t resident = int64_t(best_total / best_w) * cu_count();
+    const int64_t blocks = std::min(want, resident);
+    if (lds > 64 * 1024 &&
+        hipFuncSetAttribute(reinterpret_cast<const void *>(&decode_tiled_kernel<ELL>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
+      return false;
+    hipLaunchKernelGGL(decode_tiled_kernel<ELL>, dim3(unsigned(blocks)), dim3(best_w * kWave), lds,
+                       st, psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc);
+    return true;
+  }
   const int64_t blocks = ceil_div(P, kDecodeWaves);
   const size_t lds = sizeof(float) * ELL * m;
   hipLaunchKernelGGL(decode_kernel<ELL>, dim3(unsigned(blocks)), dim3(kDecodeThreads), lds, st,
                      psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc);
+  return true;
 }
 
 }  // namespace
@@ -276,8 +568,9 @@ extern "C" int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_
   switch (ell) {
 #define GC_CASE(E)                                                                              \
   case E:                                                                                       \
-    launch_decode<E>(psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc, \
-                     stream);                                                                   \
+    if (!launch_decode<E>(psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, \
+                          Bc, stream))                                                          \
+      return GC_ELAUNCH;                                                                        \
     break;
     GC_CASE(1) GC_CASE(2) GC_CASE(3) GC_CASE(4) GC_CASE(5) GC_CASE(6) GC_CASE(7) GC_CASE(8)
 #undef GC_CASE
