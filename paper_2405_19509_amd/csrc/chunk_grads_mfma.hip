@@ -21,6 +21,8 @@
 //   resid_kernel  U = loss'(sum of the partials, in split order) - y.
 //   utx_kernel    G tiles; both operands are row-contiguous along M and N,
 //                 held in LDS as [k][row].
+// Along the points both kernels use 128-wide tiles when b is a multiple of 128 and
+// 64-wide tiles otherwise, so b = 64 does not spend half the MFMAs on padding.
 #include "common.h"
 
 namespace gcx {
@@ -44,14 +46,17 @@ __device__ __forceinline__ float comp(const float4 &v, int e) {
   return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
 }
 
-// Z partial: Zp[s][i][r][q] = sum_{x in split s} X[i][r][x] * W[q][x]
+// Z partial: Zp[s][i][r][q] = sum_{x in split s} X[i][r][x] * W[q][x].  TB = tile width
+// along the points (128, or 64 when b is not a multiple of 128: no padded half tile).
+template <int TB>
 __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restrict__ X,
                                                           const float *__restrict__ W, int N, int n,
                                                           int64_t d, int b, int splits, int64_t kper,
                                                           int mtiles, int ntiles,
                                                           float *__restrict__ Zp) {
+  constexpr int NB = TB / 64;  // 32-wide MFMA blocks per wave along the points
   __shared__ __align__(16) float As[2][kTM][kTK + kPadK];
-  __shared__ __align__(16) float Bs[2][kTN][kTK + kPadK];
+  __shared__ __align__(16) float Bs[2][TB][kTK + kPadK];
   int64_t bid = blockIdx.x;
   const int nt = int(bid % ntiles);
   bid /= ntiles;
@@ -72,24 +77,25 @@ __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restric
     for (int p = 0; p < 4; ++p) {
       const int row = lrow + 32 * p;
       const int64_t k = kb + lk;
-      const int r = mt * kTM + row, q = nt * kTN + row;
+      const int r = mt * kTM + row, q = nt * TB + row;
       ra[p] = (r < n && k < k1) ? ld4(Xi + int64_t(r) * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-      rb[p] = (q < b && k < k1) ? ld4(W + int64_t(q) * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+      rb[p] = (row < TB && q < b && k < k1) ? ld4(W + int64_t(q) * d + k)
+                                            : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       *reinterpret_cast<float4 *>(&As[buf][lrow + 32 * p][lk]) = ra[p];
-      *reinterpret_cast<float4 *>(&Bs[buf][lrow + 32 * p][lk]) = rb[p];
+      if (lrow + 32 * p < TB) *reinterpret_cast<float4 *>(&Bs[buf][lrow + 32 * p][lk]) = rb[p];
     }
   };
 
-  v16f acc[2][2];
+  v16f acc[2][NB];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < NB; ++c)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
 
@@ -102,17 +108,18 @@ __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restric
     if (st + 1 < nst) gload(k0 + (st + 1) * kTK);
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
-      float4 a[2], bb[2];
+      float4 a[2], bb[NB];
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) a[mb] = ld4(&As[buf][wm * 64 + mb * 32 + li][h * 16 + s4 * 4]);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) bb[nb] = ld4(&Bs[buf][wn * 64 + nb * 32 + li][h * 16 + s4 * 4]);
+      for (int nb = 0; nb < NB; ++nb)
+        bb[nb] = ld4(&Bs[buf][wn * (TB / 2) + nb * 32 + li][h * 16 + s4 * 4]);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
+          for (int nb = 0; nb < NB; ++nb)
             acc[mb][nb] = mfma32(comp(a[mb], e), comp(bb[nb], e), acc[mb][nb]);
     }
     if (st + 1 < nst) lstore(buf ^ 1);
@@ -123,11 +130,11 @@ __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restric
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int r = mt * kTM + wm * 64 + mb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        const int q = nt * kTN + wn * 64 + nb * 32 + li;
+        const int q = nt * TB + wn * (TB / 2) + nb * 32 + li;
         if (r < n && q < b) Zs[int64_t(r) * b + q] = acc[mb][nb][v];
       }
 }
@@ -143,12 +150,14 @@ __global__ void resid_kernel(const float *__restrict__ Zp, const float *__restri
   Uo[e] = loss == GC_LOSS_LOGISTIC ? 1.0f / (1.0f + expf(-z)) - yv : z - yv;
 }
 
-// G[q][i][x] = sum_r U[i][r][q] * X[i][r][x]
+// G[q][i][x] = sum_r U[i][r][q] * X[i][r][x]; TB = tile height along the points.
+template <int TB>
 __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restrict__ Ui,
                                                            const float *__restrict__ X, int N, int n,
                                                            int64_t d, int b, int mtiles,
                                                            int64_t ntiles, float *__restrict__ G) {
-  __shared__ __align__(16) float As[2][kTK][kTM + 4];
+  constexpr int MB = TB / 64;  // 32-high MFMA blocks per wave along the points
+  __shared__ __align__(16) float As[2][kTK][TB + 4];
   __shared__ __align__(16) float Bs[2][kTK][kTN + 4];
   int64_t bid = blockIdx.x;
   const int mt = int(bid % mtiles);  // the point tiles of one X tile run back to back
@@ -166,23 +175,24 @@ __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restri
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       const int r = kb + lrow + 8 * p;
-      const int q = mt * kTM + lc;
+      const int q = mt * TB + lc;
       const int64_t x = nt * kTN + lc;
-      ra[p] = (r < n && q < b) ? ld4(Uc + int64_t(r) * b + q) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ra[p] = (lc < TB && r < n && q < b) ? ld4(Uc + int64_t(r) * b + q)
+                                          : make_float4(0.f, 0.f, 0.f, 0.f);
       rb[p] = (r < n && x < d) ? ld4(Xi + int64_t(r) * d + x) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      *reinterpret_cast<float4 *>(&As[buf][lrow + 8 * p][lc]) = ra[p];
+      if (lc < TB) *reinterpret_cast<float4 *>(&As[buf][lrow + 8 * p][lc]) = ra[p];
       *reinterpret_cast<float4 *>(&Bs[buf][lrow + 8 * p][lc]) = rb[p];
     }
   };
 
-  v16f acc[2][2];
+  v16f acc[MB][2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
@@ -197,13 +207,13 @@ __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restri
     if (st + 1 < nst) gload((st + 1) * kTK);
 #pragma unroll
     for (int s = 0; s < kTK / 2; ++s) {
-      float a[2], bb[2];
+      float a[MB], bb[2];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) a[mb] = As[buf][2 * s + h][wm * 64 + mb * 32 + li];
+      for (int mb = 0; mb < MB; ++mb) a[mb] = As[buf][2 * s + h][wm * (TB / 2) + mb * 32 + li];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) bb[nb] = Bs[buf][2 * s + h][wn * 64 + nb * 32 + li];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma32(a[mb], bb[nb], acc[mb][nb]);
     }
@@ -212,12 +222,12 @@ __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restri
   }
 
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int q = mt * kTM + wm * 64 + mb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+        const int q = mt * TB + wm * (TB / 2) + mb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
         const int64_t x = nt * kTN + wn * 64 + nb * 32 + li;
         if (q < b && x < d) G[(int64_t(q) * N + i) * d + x] = acc[mb][nb][v];
       }
@@ -227,6 +237,7 @@ __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restri
 
 // Launch plan shared by the workspace-size query and the launch.
 struct MfmaPlan {
+  int tb;  // tile width along the points: 128, or 64 when b is not a multiple of 128
   int splits;
   int64_t kper;
   int mtiles1, ntiles1;  // zw tiles over (rows r, points q)
@@ -235,8 +246,9 @@ struct MfmaPlan {
 
 MfmaPlan mfma_plan(int N, int n, int64_t d, int b) {
   MfmaPlan pl{};
+  pl.tb = b % 128 == 0 ? 128 : 64;
   pl.mtiles1 = int(ceil_div(n, kTM));
-  pl.ntiles1 = int(ceil_div(b, kTN));
+  pl.ntiles1 = int(ceil_div(b, pl.tb));
   const int64_t tiles = int64_t(N) * pl.mtiles1 * pl.ntiles1;
   int64_t splits = ceil_div(1536, tiles);  // about three waves of 2 blocks per CU on 256 CUs
   if (splits < 1) splits = 1;
@@ -263,18 +275,26 @@ int launch_mfma_grads(const float *X, const float *y, const float *W, int N, int
   float *Zp = static_cast<float *>(workspace);
   float *Uo = Zp + pl.zp_floats;
   const int64_t blocks1 = int64_t(N) * pl.splits * pl.mtiles1 * pl.ntiles1;
-  const int mtiles2 = int(ceil_div(b, kTM));
+  const int mtiles2 = int(ceil_div(b, pl.tb));
   const int64_t ntiles2 = ceil_div(d, kTN);
   const int64_t blocks2 = int64_t(N) * ntiles2 * mtiles2;
   const int64_t total = int64_t(N) * n * b;
   if (!grid_ok(blocks1, kMThreads) || !grid_ok(blocks2, kMThreads) || !grid_ok(ceil_div(total, 256), 256))
     return GC_EINVAL;
-  hipLaunchKernelGGL(zw_kernel, dim3(unsigned(blocks1)), dim3(kMThreads), 0, st, X, W, N, n, d, b,
-                     pl.splits, pl.kper, pl.mtiles1, pl.ntiles1, Zp);
+  if (pl.tb == 128)
+    hipLaunchKernelGGL(zw_kernel<128>, dim3(unsigned(blocks1)), dim3(kMThreads), 0, st, X, W, N, n,
+                       d, b, pl.splits, pl.kper, pl.mtiles1, pl.ntiles1, Zp);
+  else
+    hipLaunchKernelGGL(zw_kernel<64>, dim3(unsigned(blocks1)), dim3(kMThreads), 0, st, X, W, N, n,
+                       d, b, pl.splits, pl.kper, pl.mtiles1, pl.ntiles1, Zp);
   hipLaunchKernelGGL(resid_kernel, dim3(unsigned(ceil_div(total, 256))), dim3(256), 0, st, Zp, y,
                      total, b, pl.splits, loss, Uo);
-  hipLaunchKernelGGL(utx_kernel, dim3(unsigned(blocks2)), dim3(kMThreads), 0, st, Uo, X, N, n, d, b,
-                     mtiles2, ntiles2, G);
+  if (pl.tb == 128)
+    hipLaunchKernelGGL(utx_kernel<128>, dim3(unsigned(blocks2)), dim3(kMThreads), 0, st, Uo, X, N, n,
+                       d, b, mtiles2, ntiles2, G);
+  else
+    hipLaunchKernelGGL(utx_kernel<64>, dim3(unsigned(blocks2)), dim3(kMThreads), 0, st, Uo, X, N, n,
+                       d, b, mtiles2, ntiles2, G);
   return GC_OK;
 }
 
