@@ -198,21 +198,26 @@ __device__ __forceinline__ float4 gload4(const GT *__restrict__ G, int K, int64_
 // Writes the tile's estimate (if ghat) and, if red2, red2[wn][row] = squared error of the
 // row over the wave's 64 columns: each difference, square and sum of four neighbours in
 // fp32, the rest in fp64, in a fixed order.  gs = target tile [ELL][kDN] in LDS.
-template <int ELL>
+template <int ELL, bool VST>
 __device__ __forceinline__ void direct_epilogue(const v16f (&acc)[2][2], int64_t mt, int64_t nt,
-                                                int64_t rows, int64_t d, int64_t L, bool vst,
+                                                int64_t rows, int64_t d, int64_t L,
                                                 float *__restrict__ ghat, const float *gs,
                                                 double (*red2)[kDM], int wm, int wn, int h,
                                                 int li) {
   const int64_t p0 = mt * kDM / ELL;  // pattern and block of the tile's first row
   const int k0 = int(mt * kDM % ELL);
-  const bool tail = (ELL - 1) * L + (nt + 1) * kDN > d;  // the tile reaches past d somewhere
+  const int64_t x0 = nt * kDN;
+  const bool tail = (ELL - 1) * L + x0 + kDN > d;  // the tile reaches past d somewhere
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
     const int rl = wm * 64 + rb * 32 + li;
-    const int64_t r = mt * kDM + rl;
     const int64_t p = p0 + (k0 + rl) / ELL;
     const int k = (k0 + rl) % ELL;
+    // tile columns xl < lim lie inside the block (x < L) and the gradient (k*L + x < d);
+    // -1 for a row past the last pattern
+    const int lim = mt * kDM + rl < rows ? int(std::min<int64_t>(std::min(L, d - k * L) - x0, kDN)) : -1;
+    float *row = ghat ? ghat + p * d + k * L + x0 : nullptr;
+    const float *grow = gs + k * kDN;
     double rs = 0.0;
 #pragma unroll
     for (int xb = 0; xb < 2; ++xb)
@@ -221,32 +226,28 @@ __device__ __forceinline__ void direct_epilogue(const v16f (&acc)[2][2], int64_t
         const int xl = wn * 64 + xb * 32 + 8 * g + 4 * h;
         const float e0 = acc[xb][rb][4 * g], e1 = acc[xb][rb][4 * g + 1];
         const float e2 = acc[xb][rb][4 * g + 2], e3 = acc[xb][rb][4 * g + 3];
-        if (ghat && r < rows) {
-          const int64_t x = nt * kDN + xl;
-          const int64_t col = k * L + x;
-          float *dst = ghat + p * d + col;
+        if (ghat) {
           // plain stores: a wave completes each 128-byte line of a row in eight 16-byte
           // pieces, which the L2 merges before writing back
-          if (vst) {
-            if (x < L && col < d) *reinterpret_cast<v4f *>(dst) = v4f{e0, e1, e2, e3};
+          if constexpr (VST) {  // d, L multiples of 4, ghat aligned: all four in or all out
+            if (xl < lim) *reinterpret_cast<v4f *>(row + xl) = v4f{e0, e1, e2, e3};
           } else {
             const float ev[4] = {e0, e1, e2, e3};
 #pragma unroll
             for (int u = 0; u < 4; ++u)
-              if (x + u < L && col + u < d) dst[u] = ev[u];
+              if (xl + u < lim) row[xl + u] = ev[u];
           }
         }
         if (red2) {
           // past the block (x >= L) both sides hold zero; the zero-padded tail of the last
           // block (k*L + x >= d) is not part of the estimate and is masked out
-          const float4 t4 = *reinterpret_cast<const float4 *>(gs + k * kDN + xl);
+          const float4 t4 = *reinterpret_cast<const float4 *>(grow + xl);
           float d0 = e0 - t4.x, d1 = e1 - t4.y, d2 = e2 - t4.z, d3 = e3 - t4.w;
           if (tail) {
-            const int64_t col = k * L + nt * kDN + xl;
-            d0 = col < d ? d0 : 0.f;
-            d1 = col + 1 < d ? d1 : 0.f;
-            d2 = col + 2 < d ? d2 : 0.f;
-            d3 = col + 3 < d ? d3 : 0.f;
+            d0 = xl < lim ? d0 : 0.f;
+            d1 = xl + 1 < lim ? d1 : 0.f;
+            d2 = xl + 2 < lim ? d2 : 0.f;
+            d3 = xl + 3 < lim ? d3 : 0.f;
           }
           rs += double((d0 * d0 + d1 * d1) + (d2 * d2 + d3 * d3));
         }
@@ -277,7 +278,7 @@ constexpr int kDLdsA = 2 * kDM * (kDK + kDPad), kDLdsB = 2 * kDK * (kDN + 4);
 template <typename GT, bool VEC4, int ELL>
 __global__ __launch_bounds__(kDThreads, 2) void direct_kernel(
     const float *__restrict__ C, const GT *__restrict__ G, int N, int64_t d, int64_t L, int64_t Kp,
-    int64_t rows, int64_t ntiles, bool vst, float *__restrict__ ghat,
+    int64_t rows, int64_t ntiles, float *__restrict__ ghat,
     const float *__restrict__ gsum, double *__restrict__ part) {
   __shared__ __align__(16) float As[2][kDM][kDK + kDPad];
   __shared__ __align__(16) float Bs[2][kDK][kDN + 4];
@@ -353,7 +354,7 @@ __global__ __launch_bounds__(kDThreads, 2) void direct_kernel(
     __syncthreads();
   }
 
-  direct_epilogue<ELL>(acc, mt, nt, rows, d, L, vst, ghat, gs, part ? red2 : nullptr, wm, wn, h, li);
+  direct_epilogue<ELL, VEC4>(acc, mt, nt, rows, d, L, ghat, gs, part ? red2 : nullptr, wm, wn, h, li);
   if (part) {
     __syncthreads();
     const int64_t r = mt * kDM + t;
@@ -376,7 +377,7 @@ constexpr int kSLds = 2 * kSAHalf + 2 * kSBHalf + GC_MAX_ELL * kDN;  // floats; 
 template <typename GT, bool VEC4, int ELL>
 __global__ __launch_bounds__(kDThreads, 2) void direct_short_kernel(
     const float *__restrict__ C, const GT *__restrict__ G, int N, int64_t d, int64_t L, int64_t Kp,
-    int Kq, int64_t rows, int64_t ntiles, int64_t ntotal, bool vst, float *__restrict__ ghat,
+    int Kq, int64_t rows, int64_t ntiles, int64_t ntotal, float *__restrict__ ghat,
     const float *__restrict__ gsum, double *__restrict__ part) {
   __shared__ __align__(16) float smem[kSLds];
   __shared__ double red2[2][kDM];
@@ -466,8 +467,8 @@ __global__ __launch_bounds__(kDThreads, 2) void direct_short_kernel(
       acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a1, acc[1][1], 0, 0, 0);
     }
 
-    direct_epilogue<ELL>(acc, mt, nt, rows, d, L, vst, ghat, gs, part ? red2 : nullptr, wm, wn, h,
-                         li);
+    direct_epilogue<ELL, VEC4>(acc, mt, nt, rows, d, L, ghat, gs, part ? red2 : nullptr, wm, wn, h,
+                               li);
     __syncthreads();
     if (part && t < kDM) {
       const int64_t r = mt * kDM + t;
@@ -552,8 +553,9 @@ extern "C" int gc_decode_direct(const void *G, int32_t g_dtype, int32_t N, int64
     default: return GC_EINVAL;
   }
   const size_t es = g_dtype == GC_F32 ? 4 : 2;
-  const bool vec4 = d % 4 == 0 && L % 4 == 0 && (reinterpret_cast<uintptr_t>(G) % (4 * es)) == 0;
-  const bool vst = d % 4 == 0 && L % 4 == 0 && (reinterpret_cast<uintptr_t>(ghat) % 16) == 0;
+  // the VEC4 kernels load the gradients and store the estimate 16 bytes at a time
+  const bool vec4 = d % 4 == 0 && L % 4 == 0 && (reinterpret_cast<uintptr_t>(G) % (4 * es)) == 0 &&
+                    (reinterpret_cast<uintptr_t>(ghat) % 16) == 0;
   const dim3 grid{static_cast<uint32_t>(blocks)};
   const bool f32 = g_dtype == GC_F32;
   const int Kq = int(ceil_div(int64_t(N) * ell, 4) * 4);
@@ -563,11 +565,11 @@ extern "C" int gc_decode_direct(const void *G, int32_t g_dtype, int32_t N, int64
 #define GC_DIRECT(GT, V, E)                                                                        \
   if (short_k)                                                                                     \
     hipLaunchKernelGGL((direct_short_kernel<GT, V, E>), sgrid, dim3(kDThreads), 0, stream, Cm,     \
-                       static_cast<const GT *>(G), N, d, L, Kp, Kq, rows, ntiles, ntotal, vst,     \
-                       ghat, gsum, part);                                                          \
+                       static_cast<const GT *>(G), N, d, L, Kp, Kq, rows, ntiles, ntotal, ghat,    \
+                       gsum, part);                                                                \
   else                                                                                             \
     hipLaunchKernelGGL((direct_kernel<GT, V, E>), grid, dim3(kDThreads), 0, stream, Cm,            \
-                       static_cast<const GT *>(G), N, d, L, Kp, rows, ntiles, vst, ghat, gsum, part)
+                       static_cast<const GT *>(G), N, d, L, Kp, rows, ntiles, ghat, gsum, part)
 #define GC_DIRECT_ELL(E)                                                                           \
   case E:                                                                                          \
     if (f32) {                                                                                     \
