@@ -198,6 +198,83 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   }
 }
 
+// Per-worker layout, for ell >= 2 or many chunks, where the W-wide slice of every chunk
+// no longer fits in LDS at W = 256 floats: a block owns one worker j, one WW-wide slice of x
+// (WW = 1024, 512 or 256 floats: the widest whose delta*ell slices fit in kEwLds) and a
+// range of patterns, and stages only the slices of j's own delta chunks.  Consecutive
+// blocks take the slices of one row, then the next worker (the next row in memory), then
+// the next pattern range, so the blocks in flight write whole consecutive rows of T.
+// A wave writes one WW-wide row piece per transmitting pattern.
+constexpr int kEwThreads = 256;
+constexpr size_t kEwLds = 64 * 1024;   // slice budget
+constexpr int64_t kEwPatterns = 100;   // patterns per block
+
+template <typename GT, int WW>
+__global__ __launch_bounds__(kEwThreads) void encode_worker_kernel(EncodeArgs a, int64_t P,
+                                                                   int nsl) {
+  constexpr int NV = WW / (4 * kWave);  // 16-byte pieces per lane
+  extern __shared__ __align__(16) unsigned char lds[];
+  GT *Gs = reinterpret_cast<GT *>(lds);  // [delta*ell][WW]
+  const int64_t b = blockIdx.x;
+  const int s = int(b % nsl);
+  const int j = int((b / nsl) % a.m);
+  const int64_t g = b / (int64_t(nsl) * a.m);
+  const int64_t x0 = int64_t(s) * WW;
+  const int nk = a.delta * a.ell;
+  const GT *G = reinterpret_cast<const GT *>(a.G);
+  for (int e = threadIdx.x; e < nk * WW; e += kEwThreads) {
+    const int tk = e / WW, w = e % WW;
+    const int t = tk / a.ell, k = tk % a.ell;
+    const int c = a.order[int64_t(j) * a.delta + t];
+    const int64_t x = x0 + w, col = int64_t(k) * a.L + x;
+    Gs[e] = (c >= 0 && c < a.N && x < a.L && col < a.d) ? G[int64_t(c) * a.d + col] : GT(0);
+  }
+  __syncthreads();
+
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t p0 = g * kEwPatterns;
+  const int64_t p1 = p0 + kEwPatterns < P ? p0 + kEwPatterns : P;
+  for (int64_t p = p0 + wave; p < p1; p += kEwThreads / kWave) {
+    const int64_t r = p * a.m + j;
+    int np = a.psi[r];
+    np = np < 0 ? 0 : (np > a.delta ? a.delta : np);
+    if (np == 0) continue;  // a worker that has processed nothing transmits nothing
+    const float *co = a.Bc + r * nk;
+    float acc[NV][4];
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[i][q] = 0.f;
+    for (int tk = 0; tk < np * a.ell; ++tk) {  // positions in order, blocks within a position
+      const float w = co[tk];
+      const GT *src = Gs + size_t(tk) * WW + lane * 4;
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        float gv[4];
+        load_vec<GT, 4>(src + i * 4 * kWave, gv);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = fmaf(w, gv[q], acc[i][q]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int64_t x = x0 + i * 4 * kWave + lane * 4;
+      if (x < a.L) store_vec<4>(a.T + r * a.L + x, acc[i]);
+    }
+  }
+}
+
+template <typename GT, int WW>
+int launch_encode_worker(const EncodeArgs &a, int64_t P, hipStream_t st) {
+  const int nsl = int(ceil_div(a.L, WW));
+  const int64_t blocks = int64_t(nsl) * a.m * ceil_div(P, kEwPatterns);
+  if (!grid_ok(blocks, kEwThreads)) return GC_EINVAL;
+  const size_t lds = size_t(a.delta) * a.ell * WW * sizeof(GT);
+  hipLaunchKernelGGL((encode_worker_kernel<GT, WW>), dim3(unsigned(blocks)), dim3(kEwThreads), lds,
+                     st, a, P, nsl);
+  return GC_OK;
+}
+
 template <typename GT, int VEC, bool STAGE>
 int launch_encode(EncodeArgs a, hipStream_t st) {
   constexpr int W = kWave * VEC;
@@ -280,6 +357,27 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
     while (vec > 1 && (d % vec != 0 || (ga & (size_t(vec) * esize - 1)) != 0)) vec >>= 1;
   }
   (void)hipGetLastError();
+  // when the all-chunk slice cannot stay 256 wide, the per-worker layout at the widest slice
+  // (1024, 512 or 256) that fits, given 16-byte rows of T
+  if (a.L % 4 == 0 && (ta & 15) == 0 && (!stage || svec < 4)) {
+    const size_t per = size_t(delta) * ell * esize;  // LDS bytes per slice position
+    int ww = 0;
+    for (int w = 1024; w >= 256 && !ww; w >>= 1)
+      if (per * w <= kEwLds) ww = w;
+    if (ww) {
+      int st;
+      if (g_dtype == GC_F32)
+        st = ww == 1024 ? launch_encode_worker<float, 1024>(a, P, stream)
+             : ww == 512 ? launch_encode_worker<float, 512>(a, P, stream)
+                         : launch_encode_worker<float, 256>(a, P, stream);
+      else
+        st = ww == 1024 ? launch_encode_worker<uint16_t, 1024>(a, P, stream)
+             : ww == 512 ? launch_encode_worker<uint16_t, 512>(a, P, stream)
+                         : launch_encode_worker<uint16_t, 256>(a, P, stream);
+      if (st != GC_OK) return st;
+      return launch_status();
+    }
+  }
   const int st = g_dtype == GC_F32 ? dispatch_encode<float>(a, vec, stage, stream)
                                    : dispatch_encode<uint16_t>(a, vec, stage, stream);
   if (st != GC_OK) return st;
