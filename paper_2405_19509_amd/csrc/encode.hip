@@ -358,8 +358,12 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
   }
   (void)hipGetLastError();
   // when the all-chunk slice cannot stay 256 wide, the per-worker layout at the widest slice
-  // (1024, 512 or 256) that fits, given 16-byte rows of T
-  if (a.L % 4 == 0 && (ta & 15) == 0 && (!stage || svec < 4)) {
+  // (1024, 512 or 256) that fits, given 16-byte rows of T and enough patterns per block to
+  // repay the staging of each worker's slices: its staged bytes, ceil(P/100)*delta*ell*esize
+  // per row position, at most half of the 4*P bytes of T there (with very few patterns the
+  // all-chunk layout stages every chunk's slice once for all the rows)
+  const bool ew_pays = 2 * ceil_div(P, kEwPatterns) * delta * ell * int64_t(esize) <= 4 * P;
+  if (a.L % 4 == 0 && (ta & 15) == 0 && (!stage || svec < 4) && ew_pays) {
     const size_t per = size_t(delta) * ell * esize;  // LDS bytes per slice position
     int ww = 0;
     for (int w = 1024; w >= 256 && !ww; w >>= 1)
