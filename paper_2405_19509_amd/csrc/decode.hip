@@ -16,53 +16,13 @@
 #include <algorithm>
 
 #include "common.h"
+#include "small_solve.h"
 
 namespace gcx {
 namespace {
 
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeWaves = kDecodeThreads / kWave;
-
-// In-place Cholesky factorisation of a symmetric positive-definite ELL x ELL
-// matrix (lower triangle used), fully unrolled so every index is static.
-template <int ELL>
-__device__ __forceinline__ void cholesky(double (&A)[ELL][ELL]) {
-#pragma unroll
-  for (int c = 0; c < ELL; ++c) {
-    double s = A[c][c];
-#pragma unroll
-    for (int q = 0; q < c; ++q) s -= A[c][q] * A[c][q];
-    const double dcc = sqrt(s);
-    A[c][c] = dcc;
-    const double inv = 1.0 / dcc;
-#pragma unroll
-    for (int r = c + 1; r < ELL; ++r) {
-      double v = A[r][c];
-#pragma unroll
-      for (int q = 0; q < c; ++q) v -= A[r][q] * A[c][q];
-      A[r][c] = v * inv;
-    }
-  }
-}
-
-// Solve (L L^T) z = b in place, L the lower factor from cholesky().
-template <int ELL>
-__device__ __forceinline__ void chol_solve(const double (&Lf)[ELL][ELL], double (&b)[ELL]) {
-#pragma unroll
-  for (int r = 0; r < ELL; ++r) {
-    double v = b[r];
-#pragma unroll
-    for (int q = 0; q < r; ++q) v -= Lf[r][q] * b[q];
-    b[r] = v / Lf[r][r];
-  }
-#pragma unroll
-  for (int r = ELL - 1; r >= 0; --r) {
-    double v = b[r];
-#pragma unroll
-    for (int q = r + 1; q < ELL; ++q) v -= Lf[q][r] * b[q];
-    b[r] = v / Lf[r][r];
-  }
-}
 
 template <int ELL>
 __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(

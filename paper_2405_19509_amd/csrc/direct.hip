@@ -27,6 +27,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "small_solve.h"
 
 namespace gcx {
 namespace {
@@ -34,43 +35,6 @@ namespace {
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int kDM = 128, kDN = 128, kDK = 32, kDThreads = 256, kDPad = 4;
-
-template <int ELL>
-__device__ __forceinline__ void chol(double (&A)[ELL][ELL]) {
-#pragma unroll
-  for (int c = 0; c < ELL; ++c) {
-    double s = A[c][c];
-#pragma unroll
-    for (int q = 0; q < c; ++q) s -= A[c][q] * A[c][q];
-    const double dcc = sqrt(s);
-    A[c][c] = dcc;
-#pragma unroll
-    for (int r = c + 1; r < ELL; ++r) {
-      double v = A[r][c];
-#pragma unroll
-      for (int q = 0; q < c; ++q) v -= A[r][q] * A[c][q];
-      A[r][c] = v / dcc;
-    }
-  }
-}
-
-template <int ELL>
-__device__ __forceinline__ void chol_solve(const double (&Lf)[ELL][ELL], double (&b)[ELL]) {
-#pragma unroll
-  for (int r = 0; r < ELL; ++r) {
-    double v = b[r];
-#pragma unroll
-    for (int q = 0; q < r; ++q) v -= Lf[r][q] * b[q];
-    b[r] = v / Lf[r][r];
-  }
-#pragma unroll
-  for (int r = ELL - 1; r >= 0; --r) {
-    double v = b[r];
-#pragma unroll
-    for (int q = r + 1; q < ELL; ++q) v -= Lf[q][r] * b[q];
-    b[r] = v / Lf[r][r];
-  }
-}
 
 // C[(p*ell + k)*Kp + i*ell + k'] = (X X^+)[k][k'] for chunk i of pattern p.
 template <int ELL>
@@ -122,7 +86,7 @@ __global__ __launch_bounds__(256) void mix_kernel(const int32_t *__restrict__ ps
           for (int k = 0; k < ELL; ++k) v += X[k][a] * X[k][b];
           H[a][b] = (a < Delta && b < Delta) ? v : (a == b ? 1.0 : 0.0);
         }
-      chol<ELL>(H);
+      cholesky<ELL>(H);
 #pragma unroll
       for (int kk = 0; kk < ELL; ++kk) {
         double z[ELL];  // H^-1 X^T e_kk
