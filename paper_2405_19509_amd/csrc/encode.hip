@@ -93,6 +93,7 @@ struct EncodeArgs {
   int nslices;
   int64_t rows_per_block;
   int group_rows;  // rows of metadata staged per step
+  bool stage16;    // d and L multiples of 16 bytes of G, G 16-byte aligned
 };
 
 // LDS layout: [ G slice : N*ell*W GT ][ psi : group ][ chunk : group*delta ][ coef : group*delta*ell ]
@@ -125,15 +126,24 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   const int64_t r0 = rblock * a.rows_per_block;
   const int64_t r1 = r0 + a.rows_per_block < a.rows ? r0 + a.rows_per_block : a.rows;
 
-  // stage the slice: Gs[(c*ell + k)*W + w] = g_c[k*L + x0 + w] (zero past L or past d)
+  // stage the slice: Gs[(c*ell + k)*W + w] = g_c[k*L + x0 + w] (zero past L or past d),
+  // 16 bytes per load where the run lies inside the gradient (d, L and G aligned to it)
   const GT *G = reinterpret_cast<const GT *>(a.G);
   const int nrow = STAGE ? a.N * a.ell : 0;
-  for (int e = threadIdx.x; e < nrow * W; e += kEncThreads) {
-    const int ck = e / W, w = e % W;
+  constexpr int SV = 16 / sizeof(GT);
+  using SVT = uint4;
+  for (int e = threadIdx.x * SV; e < nrow * W; e += kEncThreads * SV) {
+    const int ck = e / W, w = e % W;  // W is a multiple of SV
     const int c = ck / a.ell, k = ck % a.ell;
     const int64_t x = x0 + w;
     const int64_t col = int64_t(k) * a.L + x;
-    Gs[e] = (x < a.L && col < a.d) ? G[int64_t(c) * a.d + col] : GT(0);
+    if (a.stage16 && x + SV <= a.L && col + SV <= a.d) {
+      *reinterpret_cast<SVT *>(Gs + e) = *reinterpret_cast<const SVT *>(G + int64_t(c) * a.d + col);
+    } else {
+#pragma unroll
+      for (int u = 0; u < SV; ++u)
+        Gs[e + u] = (x + u < a.L && col + u < a.d) ? G[int64_t(c) * a.d + col + u] : GT(0);
+    }
   }
 
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -346,6 +356,8 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
   // slice of every chunk in LDS when it fits, else read G through L2
   const size_t esize = g_dtype == GC_F32 ? 4 : 2;
   const uintptr_t ta = reinterpret_cast<uintptr_t>(T), ga = reinterpret_cast<uintptr_t>(G);
+  const int64_t sv = int64_t(16 / esize);
+  a.stage16 = d % sv == 0 && a.L % sv == 0 && (ga & 15) == 0;
   int vec = (a.L % 4 == 0 && (ta & 15) == 0) ? 4 : ((a.L % 2 == 0 && (ta & 7) == 0) ? 2 : 1);
   int svec = vec;
   while (svec > 1 && size_t(N) * ell * kWave * svec * esize > kEncSliceLds) svec >>= 1;
