@@ -112,6 +112,19 @@ int gc_assign(int32_t kind, int32_t N, int32_t m, int32_t s, int32_t *O, int32_t
               int32_t gamma, int32_t *order, int32_t *holder, int32_t *hpos);
 
 /*
+ * gc_qmax -- the ordering metric of Sec. 3 (host only).  For an ordering matrix
+ * O [N][m] (O[i][j] = 0 if worker j does not hold chunk i, else the 1-based
+ * position of chunk i in worker j's order; each worker's positions are
+ * 1..delta_j once each), Q_i = the most chunks the cluster can process with no
+ * copy of chunk i processed = sum over holders j of (O[i][j] - 1) + sum over the
+ * other workers of delta_j; with N = m and all loads and replications equal to
+ * delta this is the paper's sum_j O_ij + (m - delta - 1) delta.  Writes
+ * Q [N] (may be NULL) and *qmax = max_i Q_i (1 + Q_max chunks guarantee one
+ * copy of every chunk).  O, Q, qmax: host.  GC_EINVAL for an invalid O.
+ */
+int gc_qmax(const int32_t *O, int32_t N, int32_t m, int64_t *Q, int64_t *qmax);
+
+/*
  * gc_chunk_grads -- per-chunk gradients (Sec. 1: g_{D_i} is the sum over the
  * samples of chunk i of the per-sample gradient) at b evaluation points:
  *   G[q][i][:] = X_i^T r,  r = X_i w_q - y_i          (GC_LOSS_LINEAR)

@@ -192,3 +192,42 @@ extern "C" int gc_assign(int32_t kind, int32_t N, int32_t m, int32_t s, int32_t 
   }
   return GC_EINVAL;
 }
+
+// Q_i(O) (Sec. 3): the most chunks the cluster can process while no copy of D_i has been
+// processed -- every holder j of D_i stops just before it (O_ij - 1 chunks), every other
+// worker processes all of its delta_j chunks.  With N = m and every load and replication
+// equal to delta this is the paper's sum_j O_ij + (m - delta - 1) delta over the holders.
+extern "C" int gc_qmax(const int32_t *O, int32_t N, int32_t m, int64_t *Q, int64_t *qmax) {
+  if (N < 1 || m < 1 || m > GC_MAX_M || !O || !qmax) return GC_EINVAL;
+  std::vector<int64_t> load(m, 0);
+  std::vector<std::vector<char>> seen(m);
+  for (int32_t j = 0; j < m; ++j) {
+    for (int32_t i = 0; i < N; ++i) {
+      const int32_t o = O[int64_t(i) * m + j];
+      if (o < 0 || o > N) return GC_EINVAL;
+      if (o > 0) ++load[j];
+    }
+    // the positions of a worker are 1..delta_j, once each
+    seen[j].assign(size_t(load[j]) + 1, 0);
+    for (int32_t i = 0; i < N; ++i) {
+      const int32_t o = O[int64_t(i) * m + j];
+      if (o == 0) continue;
+      if (o > load[j] || seen[j][o]) return GC_EINVAL;
+      seen[j][o] = 1;
+    }
+  }
+  int64_t total = 0;
+  for (int32_t j = 0; j < m; ++j) total += load[j];
+  int64_t best = -1;
+  for (int32_t i = 0; i < N; ++i) {
+    int64_t q = total;  // everyone finishes ...
+    for (int32_t j = 0; j < m; ++j) {
+      const int32_t o = O[int64_t(i) * m + j];
+      if (o > 0) q -= load[j] - (o - 1);  // ... except the holders of D_i, who stop before it
+    }
+    if (Q) Q[i] = q;
+    if (q > best) best = q;
+  }
+  *qmax = best;
+  return GC_OK;
+}

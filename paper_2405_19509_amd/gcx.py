@@ -34,6 +34,7 @@ SIGNATURES = {
     "gc_version": (_c.c_int, []),
     "gc_strerror": (_c.c_char_p, [_c.c_int]),
     "gc_assign": (_c.c_int, [_i32, _i32, _i32, _i32, _p, _i32, _i32, _p, _p, _p]),
+    "gc_qmax": (_c.c_int, [_p, _i32, _i32, _p, _p]),
     "gc_chunk_grads_workspace_size": (_sz, [_i32, _i32, _i64, _i32]),
     "gc_chunk_grads": (_c.c_int, [_p, _p, _p, _i32, _i32, _i64, _i32, _i32, _p, _p, _sz, _p]),
     "gc_sum_chunks": (_c.c_int, [_p, _i32, _i32, _i64, _p, _p]),
@@ -149,6 +150,16 @@ def gc_assign(kind: int, N: int, m: int, s: int = -1, O: Optional[np.ndarray] = 
                        holder.ctypes.data, hpos.ctypes.data)
     _check("gc_assign", st)
     return O, order, holder, hpos
+
+
+def gc_qmax(O):
+    """O [N][m] ordering matrix (host) -> (Q [N] int64, Q_max): the Sec. 3 metric."""
+    O = np.ascontiguousarray(O, dtype=np.int32)
+    N, m = O.shape
+    Q = np.empty(N, dtype=np.int64)
+    qmax = ctypes.c_int64(0)
+    _check("gc_qmax", load().gc_qmax(O.ctypes.data, N, m, Q.ctypes.data, ctypes.byref(qmax)))
+    return Q, int(qmax.value)
 
 
 def gc_chunk_grads_workspace_size(N: int, n: int, d: int, b: int) -> int:

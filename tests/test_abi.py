@@ -166,3 +166,42 @@ def test_assign_regular_rejects_irregular():
     assert _raw_assign(gcx.GC_ASSIGN_REGULAR, 5, 5, -1, S, 1, 1) == gcx.GC_EINVAL
     S2 = np.ones((4, 5), dtype=np.int32)          # N != m
     assert _raw_assign(gcx.GC_ASSIGN_REGULAR, 4, 5, -1, S2, 5, 4) == gcx.GC_EINVAL
+
+
+def test_qmax_matches_the_oracle():
+    """gc_qmax (the Sec. 3 ordering metric) against the oracle's direct count, on cyclic codes,
+    random orderings of random regular supports, Algorithm 2 orderings (where every row of O
+    sums to delta(delta+1)/2, so Q_max = delta(delta+1)/2 + (m - delta - 1) delta) and a
+    non-square assignment; invalid orderings are rejected."""
+    import oracle.ordering as OO
+    import pins
+    g = np.random.default_rng(21)
+    for m, s in [(6, 2), (20, 3), (50, 4), (200, 7)]:
+        O = OA.cyclic_O(m, m, s)
+        Q, qm = gcx.gc_qmax(O)
+        assert (Q == OA.Q(O)).all() and qm == OO.q_max(O)
+    for m, delta in [(12, 3), (40, 5), (200, 8)]:
+        S = pins._random_regular_support(g, m, delta)
+        for _ in range(3):
+            O = np.zeros((m, m), dtype=np.int64)
+            for j in range(m):
+                rows = np.flatnonzero(S[:, j])
+                O[rows, j] = g.permutation(delta) + 1
+            Q, qm = gcx.gc_qmax(O)
+            assert (Q == OA.Q(O)).all() and qm == OO.q_max(O)
+        O2, _, _, _ = gcx.gc_assign(gcx.GC_ASSIGN_REGULAR, m, m, -1, S.astype(np.int32), delta, delta)
+        _, qm = gcx.gc_qmax(O2)
+        assert qm == delta * (delta + 1) // 2 + (m - delta - 1) * delta
+    O = pins.sec2_2_O()                           # unequal loads (the Sec. 2.2 example)
+    assert (gcx.gc_qmax(O)[0] == OA.Q(O)).all()
+    O = np.zeros((7, 5), dtype=np.int64)          # N = 7 chunks over m = 5 workers
+    nxt = np.zeros(5, dtype=np.int64)
+    for i in range(7):
+        for j in (i % 5, (i + 2) % 5):
+            nxt[j] += 1
+            O[i, j] = nxt[j]
+    assert (gcx.gc_qmax(O)[0] == OA.Q(O)).all()
+    bad = OA.cyclic_O(6, 6, 2).copy()
+    bad[0, 0] = 2                                  # two chunks at position 2 of worker 0
+    with pytest.raises(gcx.GcxError):
+        gcx.gc_qmax(bad)

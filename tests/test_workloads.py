@@ -71,3 +71,15 @@ def test_given_gradients_and_bf16_rounding():
     R1 = gen.shared_R(50, 1)
     R2 = gen.shared_R(50, 2)
     assert np.array_equal(R1[0], R2[0]) and R2.dtype == np.float32
+
+
+def test_random_orderings_are_orderings_of_the_support():
+    A = gen.random_regular_graph(40, 5)
+    Os = gen.random_orderings(A, 7, seed=3)
+    assert Os.shape == (7, 40, 40)
+    for O in Os:
+        assert ((O != 0) == (A != 0)).all()
+        for j in range(40):
+            assert sorted(O[:, j][O[:, j] != 0]) == [1, 2, 3, 4, 5]
+    assert not (Os[0] == Os[1]).all()
+    assert (gen.random_orderings(A, 7, seed=3) == Os).all()

@@ -11,6 +11,8 @@ so that changing one size never changes another quantity's values:
     spawn key (5, 0)   per-worker speed factors (heterogeneous model)
     spawn key (5, 1+b) straggler patterns of batch b (PATTERN_BATCH patterns)
     spawn key (6, m, nu) random nu-regular graphs on m vertices (regular-graph assignments)
+    spawn key (7, trials, m) chunk times and failed workers of the Sec. 4 simulations
+    spawn key (8, count, N, m) random within-worker chunk orderings
 
 Straggler patterns follow the simulation model of the paper's numerical
 section: a worker processes its chunks in its fixed order, one chunk at a time,
@@ -264,6 +266,20 @@ def random_regular_graph(m: int, nu: int, seed: int = 0, attempt_limit: int = 10
         if ok:
             return A
     raise RuntimeError("no simple regular graph found")
+
+
+def random_orderings(A: np.ndarray, count: int, seed: int = 0) -> np.ndarray:
+    """count ordering matrices [count][N][m] on the support A: every worker processes its
+    chunks in an independent uniformly random order (positions 1..load of the worker)."""
+    A = np.asarray(A) != 0
+    N, m = A.shape
+    rng = _rng(seed, 8, count, N, m)
+    out = np.zeros((count, N, m), dtype=np.int32)
+    for c in range(count):
+        for j in range(m):
+            rows = np.flatnonzero(A[:, j])
+            out[c, rows, j] = rng.permutation(len(rows)) + 1
+    return out
 
 
 def chunk_times(wl: Workload, trials: int, seed: int = 0, failed: int | None = None):
