@@ -222,13 +222,18 @@ template <int ELL>
 struct DecodeLayout {
   static constexpr int NF = ELL * (ELL + 1) / 2;  // packed lower triangle
   // words (4 bytes) of the block-shared part and of one wave's region
-  __host__ __device__ static int64_t shared_words(int N, int m, int gamma) {
-    return (2 * int64_t(gamma) * N + m + int64_t(ELL) * m + 3) & ~int64_t(3);
+  // tables [gamma][N] x 2, loads [m], Rs [ELL][m] + a zero for the sentinel worker m,
+  // and with Bc the order table [m][delta] (entries past the chunks: the sentinel chunk N)
+  __host__ __device__ static int64_t shared_words(int N, int m, int gamma, int delta, bool bc) {
+    const int64_t ord = bc ? int64_t(m) * delta : 0;
+    return (2 * int64_t(gamma) * N + m + int64_t(ELL) * m + 1 + ord + 3) & ~int64_t(3);
   }
+  // F [N + 1][NF] doubles (row N: the sentinel chunk, zero), covS [N + 1], sel [N][ELL]
+  // (ell > 1), psi [m + 1] (entry m: the sentinel worker)
   __host__ __device__ static int64_t wave_words(int N, int m, bool bc) {
-    const int64_t f = bc ? 2 * int64_t(N) * NF : 0;        // doubles
+    const int64_t f = bc ? 2 * int64_t(N + 1) * NF : 0;
     const int64_t sel = (bc && ELL > 1) ? int64_t(N) * ELL : 0;
-    return (f + N + sel + m + 3) & ~int64_t(3);
+    return (f + N + 1 + sel + m + 1 + 3) & ~int64_t(3);
   }
 };
 
@@ -248,12 +253,17 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
   int32_t *holdT = sh;                           // [gamma][N]
   int32_t *hposT = holdT + int64_t(gamma) * N;   // [gamma][N]
   int32_t *loads = hposT + int64_t(gamma) * N;   // [m]
-  float *Rs = reinterpret_cast<float *>(loads + m);  // [ELL][m]
+  float *Rs = reinterpret_cast<float *>(loads + m);  // [ELL][m] + 1
+  int32_t *ordS = reinterpret_cast<int32_t *>(Rs + ELL * m + 1);  // [m][delta] (with Bc)
   const bool want_bc = Bc != nullptr;
+  // table entries outside [0, m) x [0, delta) point at the sentinel worker m, whose psi
+  // entry is -1 (never past any position) and whose weight is 0
   for (int e = threadIdx.x; e < N * gamma; e += blockDim.x) {
     const int i = e / gamma, u = e % gamma;
-    holdT[int64_t(u) * N + i] = holder[e];
-    hposT[int64_t(u) * N + i] = hpos[e];
+    const int j = holder[e], t = hpos[e];
+    const bool ok = j >= 0 && j < m && t >= 0 && t < delta;
+    holdT[int64_t(u) * N + i] = ok ? j : m;
+    hposT[int64_t(u) * N + i] = ok ? t : 0;
   }
   for (int j = threadIdx.x; j < m; j += blockDim.x) {
     int load = 0;
@@ -263,18 +273,33 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
     }
     loads[j] = load;
   }
-  if (want_bc)
+  if (want_bc) {
     for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
+    if (threadIdx.x == 0) Rs[ELL * m] = 0.f;
+    for (int e = threadIdx.x; e < m * delta; e += blockDim.x) {
+      const int c = order[e];
+      ordS[e] = (c >= 0 && c < N) ? c : N;
+    }
+  }
   __syncthreads();  // the only block barrier; every thread reaches it
 
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const int nw = blockDim.x / kWave;
-  int32_t *region = sh + Lay::shared_words(N, m, gamma) + int64_t(wave) * Lay::wave_words(N, m, want_bc);
-  double *F = reinterpret_cast<double *>(region);                  // [N][NF]
-  int32_t *covS = region + (want_bc ? 2 * int64_t(N) * NF : 0);    // [N]
-  int32_t *sel = covS + N;                                          // [N][ELL] (ELL > 1)
+  int32_t *region = sh + Lay::shared_words(N, m, gamma, delta, want_bc) +
+                    int64_t(wave) * Lay::wave_words(N, m, want_bc);
+  double *F = reinterpret_cast<double *>(region);                      // [N + 1][NF]
+  int32_t *covS = region + (want_bc ? 2 * int64_t(N + 1) * NF : 0);    // [N + 1]
+  int32_t *sel = covS + N + 1;                                          // [N][ELL] (ELL > 1)
   int32_t *pss = sel + ((want_bc && ELL > 1) ? int64_t(N) * ELL : 0);  // [m]
   const int64_t wstride = int64_t(delta) * ELL;
+  // phase 2 walks e = lane, lane + 64, ... as (worker, position) = (e / delta, e % delta)
+  const int j_first = lane / delta, t_first = lane % delta;
+  const int j_step = kWave / delta, t_step = kWave % delta;
+  if (want_bc && lane == 0) {  // the sentinel chunk: no coverage, zero coefficients
+    covS[N] = 0;
+#pragma unroll
+    for (int a = 0; a < NF; ++a) F[int64_t(N) * NF + a] = 0.0;
+  }
 
   for (int64_t p = int64_t(blockIdx.x) * nw + wave; p < P; p += int64_t(gridDim.x) * nw) {
     bool bad = false;
@@ -283,6 +308,7 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
       pss[j] = v;
       bad = bad || v < 0 || v > loads[j];
     }
+    if (lane == 0) pss[m] = -1;
     const bool invalid = __any(bad);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -295,14 +321,13 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
       int Delta = 0;
       double ss = 0.0;  // ell = 1: sum of R_j^2 over the members, in holder order
 #pragma unroll 4
-      for (int u = 0; u < gamma; ++u) {
+      for (int u = 0; u < gamma; ++u) {  // branch-free: non-members add 0
         const int j = holdT[u * N + i], t = hposT[u * N + i];
-        if (j >= 0 && j < m && t >= 0 && t < delta && pss[j] > t) {
-          ++Delta;
-          if (ELL == 1 && want_bc) {
-            const double x = Rs[j];
-            ss += x * x;
-          }
+        const bool member = pss[j] > t;
+        Delta += member ? 1 : 0;
+        if (ELL == 1 && want_bc) {
+          const double x = Rs[j];
+          ss += member ? x * x : 0.0;
         }
       }
       if (cov != nullptr) cov[p * N + i] = Delta;
@@ -327,7 +352,7 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
           for (int b = 0; b < ELL; ++b) M[a][b] = 0.0;
         for (int u = 0; u < gamma; ++u) {
           const int j = holdT[u * N + i], t = hposT[u * N + i];
-          if (j >= 0 && j < m && t >= 0 && t < delta && pss[j] > t) {
+          if (pss[j] > t) {
             double x[ELL];
 #pragma unroll
             for (int k = 0; k < ELL; ++k) x[k] = Rs[k * m + j];
@@ -349,7 +374,7 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
         int cnt = 0;
         for (int u = 0; u < gamma; ++u) {
           const int j = holdT[u * N + i], t = hposT[u * N + i];
-          if (j >= 0 && j < m && t >= 0 && t < delta && pss[j] > t) {
+          if (pss[j] > t) {
 #pragma unroll
             for (int a = 0; a < ELL; ++a)
               if (a == cnt) selj[a] = j;
@@ -395,68 +420,101 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
 
     // ---- phase 2: one lane per coefficient row (j, t), Bc order
     float *Bp = Bc + p * int64_t(m) * wstride;
-#pragma unroll 4
-    for (int e = lane; e < m * delta; e += kWave) {
-      const int j = e / delta, t = e % delta;
-      const int c = order[e];
-      float out[ELL];
+    const int nrow = m * delta;
+    if (ELL == 1 && delta >= 4 && (nrow & 3) == 0 && (reinterpret_cast<uintptr_t>(Bp) & 15) == 0) {
+      // four consecutive rows per lane, one 16-byte store
+      int j4 = (4 * lane) / delta, t4 = (4 * lane) % delta;
+      const int j4_step = (4 * kWave) / delta, t4_step = (4 * kWave) % delta;
+      for (int e0 = 4 * lane; e0 < nrow; e0 += 4 * kWave) {
+        float o[4];
+        int jj = j4, tt = t4;
 #pragma unroll
-      for (int k = 0; k < ELL; ++k) out[k] = 0.f;
-      const bool valid = c >= 0 && c < N && pss[j] > t;
-      if constexpr (ELL == 1) {
-        if (valid && F[c] != 0.0) out[0] = float(double(Rs[j]) * F[c]);  // +0 otherwise
-      }
-      const int Delta = (ELL > 1 && valid) ? covS[c] : 0;
-      if (ELL > 1 && !invalid && Delta > 0) {
-        const double *Fc = F + int64_t(c) * NF;
-        if constexpr (ELL == 1) {
-        } else if (Delta >= ELL) {
-          double Lf[ELL][ELL];
-#pragma unroll
-          for (int a = 0; a < ELL; ++a)
-#pragma unroll
-            for (int b = 0; b < ELL; ++b) Lf[a][b] = b <= a ? Fc[a * (a + 1) / 2 + b] : 0.0;
-          double cc[ELL];
-#pragma unroll
-          for (int k = 0; k < ELL; ++k) cc[k] = Rs[k * m + j];
-          chol_solve<ELL>(Lf, cc);
-#pragma unroll
-          for (int k = 0; k < ELL; ++k) out[k] = float(cc[k]);
-        } else {
-          double Lf[ELL][ELL];
-#pragma unroll
-          for (int a = 0; a < ELL; ++a)
-#pragma unroll
-            for (int b = 0; b < ELL; ++b) Lf[a][b] = b <= a ? Fc[a * (a + 1) / 2 + b] : 0.0;
-          int selj[ELL];
-          int me = 0;  // j's place among the members
-#pragma unroll
-          for (int a = 0; a < ELL; ++a) {
-            selj[a] = sel[int64_t(c) * ELL + a];
-            if (a < Delta && selj[a] == j) me = a;
-          }
-          double X[ELL][ELL];
-#pragma unroll
-          for (int a = 0; a < ELL; ++a) {
-            const int ja = a < Delta ? selj[a] : 0;
-#pragma unroll
-            for (int k = 0; k < ELL; ++k) X[k][a] = a < Delta ? double(Rs[k * m + ja]) : 0.0;
-          }
-          double z[ELL];
-#pragma unroll
-          for (int b = 0; b < ELL; ++b) z[b] = (me == b) ? 1.0 : 0.0;
-          chol_solve<ELL>(Lf, z);
-#pragma unroll
-          for (int k = 0; k < ELL; ++k) {
-            double v = 0.0;
-#pragma unroll
-            for (int b = 0; b < ELL; ++b) v += z[b] * X[k][b];
-            out[k] = float(v);
+        for (int q = 0; q < 4; ++q) {
+          const double f = F[ordS[e0 + q]];  // zero for the sentinel chunk, Delta = 0, invalid
+          o[q] = (pss[jj] > tt && f != 0.0) ? float(double(Rs[jj]) * f) : 0.f;
+          if (++tt == delta) {
+            tt = 0;
+            ++jj;
           }
         }
+        *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
+        j4 += j4_step;
+        t4 += t4_step;
+        if (t4 >= delta) {
+          t4 -= delta;
+          ++j4;
+        }
       }
-#pragma unroll
-      for (int k = 0; k < ELL; ++k) Bp[int64_t(e) * ELL + k] = out[k];
+    } else {
+      int j = j_first, t = t_first;
+  #pragma unroll 4
+      for (int e = lane; e < nrow; e += kWave) {
+        const int c = ordS[e];
+        float out[ELL];
+  #pragma unroll
+        for (int k = 0; k < ELL; ++k) out[k] = 0.f;
+        const bool valid = c < N && pss[j] > t;
+        if constexpr (ELL == 1) {
+          if (valid && F[c] != 0.0) out[0] = float(double(Rs[j]) * F[c]);  // +0 otherwise
+        }
+        const int Delta = (ELL > 1 && valid) ? covS[c] : 0;
+        if (ELL > 1 && !invalid && Delta > 0) {
+          const double *Fc = F + int64_t(c) * NF;
+          if constexpr (ELL == 1) {
+          } else if (Delta >= ELL) {
+            double Lf[ELL][ELL];
+  #pragma unroll
+            for (int a = 0; a < ELL; ++a)
+  #pragma unroll
+              for (int b = 0; b < ELL; ++b) Lf[a][b] = b <= a ? Fc[a * (a + 1) / 2 + b] : 0.0;
+            double cc[ELL];
+  #pragma unroll
+            for (int k = 0; k < ELL; ++k) cc[k] = Rs[k * m + j];
+            chol_solve<ELL>(Lf, cc);
+  #pragma unroll
+            for (int k = 0; k < ELL; ++k) out[k] = float(cc[k]);
+          } else {
+            double Lf[ELL][ELL];
+  #pragma unroll
+            for (int a = 0; a < ELL; ++a)
+  #pragma unroll
+              for (int b = 0; b < ELL; ++b) Lf[a][b] = b <= a ? Fc[a * (a + 1) / 2 + b] : 0.0;
+            int selj[ELL];
+            int me = 0;  // j's place among the members
+  #pragma unroll
+            for (int a = 0; a < ELL; ++a) {
+              selj[a] = sel[int64_t(c) * ELL + a];
+              if (a < Delta && selj[a] == j) me = a;
+            }
+            double X[ELL][ELL];
+  #pragma unroll
+            for (int a = 0; a < ELL; ++a) {
+              const int ja = a < Delta ? selj[a] : 0;
+  #pragma unroll
+              for (int k = 0; k < ELL; ++k) X[k][a] = a < Delta ? double(Rs[k * m + ja]) : 0.0;
+            }
+            double z[ELL];
+  #pragma unroll
+            for (int b = 0; b < ELL; ++b) z[b] = (me == b) ? 1.0 : 0.0;
+            chol_solve<ELL>(Lf, z);
+  #pragma unroll
+            for (int k = 0; k < ELL; ++k) {
+              double v = 0.0;
+  #pragma unroll
+              for (int b = 0; b < ELL; ++b) v += z[b] * X[k][b];
+              out[k] = float(v);
+            }
+          }
+        }
+  #pragma unroll
+        for (int k = 0; k < ELL; ++k) Bp[int64_t(e) * ELL + k] = out[k];
+        j += j_step;
+        t += t_step;
+        if (t >= delta) {
+          t -= delta;
+          ++j;
+        }
+      }
     }
     // the next pattern overwrites this wave's region only after every lane is done with it
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -473,7 +531,7 @@ bool launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *o
                    int32_t *cov, uint8_t *dec, int32_t *coef_err, float *Bc, hipStream_t st) {
   using Lay = DecodeLayout<ELL>;
   const bool bc = Bc != nullptr;
-  const size_t shared = 4 * size_t(Lay::shared_words(N, m, gamma));
+  const size_t shared = 4 * size_t(Lay::shared_words(N, m, gamma, delta, bc));
   const size_t per_wave = 4 * size_t(Lay::wave_words(N, m, bc));
   // the most waves per CU the LDS allows (at most 32), in blocks of up to 16 waves
   int best_w = 0, best_total = 0;
