@@ -291,6 +291,16 @@ int gc_original_ls(const int32_t *psi, int64_t P, int32_t N, int32_t m, const in
                    int32_t delta, const int32_t *holder, int32_t gamma, int32_t max_iter,
                    double tol, double *err, int32_t *iters, hipStream_t stream);
 
+/*
+ * gc_hbm_probe -- calibration, not a step of the method: streams over `bytes`
+ * bytes of buf (device, 16-byte aligned) with one 4 KB piece per block, blocks
+ * in order, writing constants (mode 0, non-temporal 16-byte stores) or reading
+ * (mode 1, non-temporal 16-byte loads; sink: one device float, written only for
+ * a value finite data never produce).  Timing it gives the streaming bandwidth
+ * this device delivers, the practical ceiling of the HBM-bound kernels.
+ */
+int gc_hbm_probe(void *buf, size_t bytes, int32_t mode, float *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

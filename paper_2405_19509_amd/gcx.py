@@ -46,6 +46,7 @@ SIGNATURES = {
     "gc_original_ls": (_c.c_int, [_p, _i64, _i32, _i32, _p, _i32, _p, _i32, _i32, _c.c_double, _p, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
+    "gc_hbm_probe": (_c.c_int, [_p, _sz, _i32, _p, _p]),
     "gc_decode_direct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_decode_direct": (_c.c_int, [_p, _i32, _i32, _i64, _p, _i64, _i32, _i32, _p, _p, _i32, _p,
                                     _i32, _p, _p, _p, _p, _sz, _p]),
@@ -283,6 +284,18 @@ def gc_reconstruct(T, R, d: int, psi=None, ghat=None, gsum=None, sqerr=None, wan
         ws_ptr, ws_bytes, _stream(stream))
     _check("gc_reconstruct", st)
     return ghat, sqerr
+
+
+def gc_hbm_probe(buf, nbytes: int, mode: int, sink=None, stream=None):
+    """Calibration stream over the first nbytes of a device tensor: mode 0 writes, 1 reads."""
+    torch = _torch()
+    if nbytes > buf.numel() * buf.element_size():
+        raise ValueError("nbytes exceeds the buffer")
+    if mode == 1 and sink is None:
+        sink = torch.zeros(1, dtype=torch.float32, device=buf.device)
+    _check("gc_hbm_probe", load().gc_hbm_probe(buf.data_ptr(), nbytes, mode,
+                                               _dev(sink, "sink", torch.float32) if sink is not None else None,
+                                               _stream(stream)))
 
 
 def gc_decode_direct_workspace_size(P: int, N: int, d: int, ell: int) -> int:

@@ -119,6 +119,11 @@ def test_device_calls_validate_on_the_host():
     assert direct(ws=p + 4) == E                                        # unaligned workspace
     assert direct(holder=None) == E and direct(G=None) == E
     assert direct(P=0) == gcx.GC_OK
+    assert lib.gc_hbm_probe(None, 4096, 0, None, None) == E                                   # null
+    assert lib.gc_hbm_probe(p + 4, 4096, 0, None, None) == E                                  # unaligned
+    assert lib.gc_hbm_probe(p, 4096, 2, None, None) == E                                      # mode
+    assert lib.gc_hbm_probe(p, 4096, 1, None, None) == E                                      # read w/o sink
+    assert lib.gc_hbm_probe(p, 8, 0, None, None) == E                                         # too small
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 5, p, p, 1 << 20, None) == E                # loss
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 0, p, p, 4, None) == E                      # small ws
     assert lib.gc_sum_chunks(p, 3, 2, 8, p, None) == E
