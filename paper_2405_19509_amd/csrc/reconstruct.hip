@@ -7,7 +7,7 @@
 // every worker's row); consecutive blocks take consecutive pieces, so the
 // blocks in flight sweep each pattern's T rows as adjacent 4 KB pieces, the
 // read shape that measured fastest on MI355X.  Each thread holds one
-// float4 of ell accumulators and keeps UNR rows of loads in flight;
+// float4 of ell accumulators and keeps kRecUnroll rows of loads in flight;
 // R[k][j] is a wave-uniform (scalar) load.  T is read with non-temporal
 // loads (it is consumed once).  The squared error is accumulated in fp64 per
 // block and reduced across pieces in a fixed order by a second small kernel,
@@ -20,7 +20,7 @@ namespace {
 
 constexpr int kRecThreads = 256;
 constexpr int64_t kRecPiece = 1024;  // x positions per block
-constexpr int kRecUnroll = 4;        // rows of T loads in flight per thread
+constexpr int kRecUnroll = 8;        // rows of T loads in flight per thread
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
