@@ -234,6 +234,71 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     assert (host(sq2) == sqerr).all()
 
 
+def _uneven_assignment(seed=5):
+    """9 chunks over 6 workers, 2 or 3 holders per chunk, loads 3 to 5, orders shuffled."""
+    N, m = 9, 6
+    g = np.random.default_rng(seed)
+    S = np.zeros((N, m), dtype=bool)
+    for i in range(N):
+        S[i, [i % m, (i + 2) % m]] = True
+        if i % 3 == 0:
+            S[i, (i + 3) % m] = True
+    O = np.zeros((N, m), dtype=np.int32)
+    for j in range(m):
+        rows = np.flatnonzero(S[:, j])
+        O[rows, j] = g.permutation(len(rows)) + 1
+    return O
+
+
+@pytest.mark.parametrize("ell", [1, 2])
+def test_uneven_non_square_assignment(ell):
+    """N != m with unequal loads and replications, through GC_ASSIGN_ORDER: coefficients,
+    encode, combine and the PS-side estimate against the oracle on every valid psi drawn."""
+    O = _uneven_assignment()
+    N, m = O.shape
+    _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, N, m, -1, O)
+    loads = (O != 0).sum(axis=0)
+    g = np.random.default_rng(11 + ell)
+    # 40 patterns uniform over each worker's progress, 20 with every worker at most one short
+    psi = np.concatenate([np.stack([g.integers(0, loads + 1) for _ in range(40)]),
+                          np.maximum(loads - g.integers(0, 2, size=(20, m)), 0)]).astype(np.int32)
+    R = gen.shared_R(m, ell)
+    d = 301
+    G = g.standard_normal((N, d)).astype(np.float32)
+    cov, dec, cerr, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+    cov, dec, cerr = host(cov), host(dec), host(cerr)
+    for p in range(len(psi)):
+        c = OP.coverage(O, psi[p])
+        assert (cov[p] == c).all() and dec[p] == int((c >= ell).all())
+        assert cerr[p] == OP.coef_err(O, psi[p], ell)
+    Bc_ref, kappa = R_.coefficients(O, psi, R)
+    assert (np.abs(host(Bc).astype(np.float64) - Bc_ref) <= R_.bc_bound(Bc_ref, kappa, O)).all()
+    # encode + combine on the oracle's coefficients
+    Bc32 = Bc_ref.astype(np.float32)
+    T = host(gcx.gc_encode(dev(G), dev(psi), dev(order), dev(Bc32)))
+    T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, G.astype(np.float64), ell)
+    sent = psi > 0
+    assert (np.abs(T[sent] - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    T32 = T_ref.astype(np.float32)
+    gh, _ = gcx.gc_reconstruct(dev(T32), dev(R), d, psi=dev(psi))
+    gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, d)
+    assert (np.abs(host(gh) - gh_ref) <= R_.gamma(m) * mag).all()
+    # the PS-side estimate from the chunk gradients
+    G64 = G.astype(np.float64)
+    gsum = G64.sum(axis=0).astype(np.float32)
+    ghd, sq = gcx.gc_decode_direct(dev(G), dev(psi), dev(order), dev(holder), dev(hpos), dev(R),
+                                   gsum=dev(gsum))
+    ghd, sq = host(ghd).astype(np.float64), host(sq)
+    ref, mg, kap = R_.direct_ref(O, psi, R, G64)
+    magG = np.tile(np.abs(R_.gblocks(G64, ell)).sum(axis=(0, 1)), ell)[:d]
+    bound = 2 * R_.gamma(N * ell + 2) * mg + 1e-13 * (kap ** 2)[:, None] * magG
+    assert (np.abs(ghd - ref) <= bound + 1e-30).all()
+    # sqerr against the GPU's own estimate (fp32 differences, fp64 sum)
+    se = ((ghd - gsum.astype(np.float64)) ** 2).sum(axis=1)
+    assert np.allclose(sq, se, rtol=1e-5, atol=1e-9)
+    assert (dec == (np.abs(ghd - gsum).max(axis=1) <= 1e-3 * np.abs(gsum).max())).all()
+
+
 def test_sum_chunks():
     for wl in (TINY, RAGGED, RAGGED_BF16, LARGE_D16):
         G = _data_G(wl)
