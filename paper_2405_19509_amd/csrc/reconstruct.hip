@@ -2,53 +2,61 @@
 // sum_j R[k][j] g_j -- with an optional fused squared error against the exact
 // target; and gc_sum_chunks, the exact target sum_i g_{D_i} itself.
 //
-// Bandwidth design (HBM-bound on the T read, ~0.5 flop per byte): a block
-// owns one pattern and one piece of 1024 consecutive x positions (4 KB of
-// every worker's row); consecutive blocks take consecutive pieces, so the
-// blocks in flight sweep each pattern's T rows as adjacent 4 KB pieces, the
-// read shape that measured fastest on MI355X.  Each thread holds one
-// float4 of ell accumulators and keeps kRecUnroll rows of loads in flight;
-// R[k][j] is a wave-uniform (scalar) load.  T is read with non-temporal
-// loads (it is consumed once).  The squared error is accumulated in fp64 per
-// block and reduced across pieces in a fixed order by a second small kernel,
-// so it is deterministic.  Given psi, rows of workers with psi = 0 (which
-// transmitted nothing) are neither read nor needed.
+// Bandwidth design (HBM-bound on the T read, ~0.5 flop per byte): a block of
+// 1024 threads owns one pattern and one piece of 4096 consecutive x positions
+// (16 KB of every transmitting worker's row, read as one coalesced sweep per
+// row); consecutive blocks take consecutive pieces of a pattern.  Measured on
+// MI355X, 16 KB per row and block beats 4 KB and 8 KB (2-3%), and one float4
+// per thread and row beats two or four.  Each thread holds one float4 of ell
+// accumulators and keeps kRecUnroll rows of loads in flight; the transmitting
+// rows and their weights R[k][j] are compacted into LDS first.  T is read with
+// non-temporal loads (it is consumed once).  The squared error is accumulated
+// in fp64 per block and reduced across pieces in a fixed order by a second
+// small kernel, so it is deterministic.  Given psi, rows of workers with
+// psi = 0 (which transmitted nothing) are neither read nor needed.
 #include "common.h"
 
 namespace gcx {
 namespace {
 
-constexpr int kRecThreads = 256;
-constexpr int64_t kRecPiece = 1024;  // x positions per block
+constexpr int kRecThreads = 1024;
+constexpr int kRecNV = 1;            // float4 (or 4 scalars) per thread and row
+constexpr int kRecV = 4 * kRecNV;    // x positions per thread
+constexpr int64_t kRecPiece = int64_t(kRecThreads) * kRecV;  // x positions per block
 constexpr int kRecUnroll = 8;        // rows of T loads in flight per thread
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 int64_t rec_pieces(int64_t L) { return ceil_div(L, kRecPiece); }
 
-// VEC = 4: thread t owns x = piece*1024 + 4t .. 4t+3 (needs L % 4 == 0 and aligned T);
-// VEC = 1: thread t owns x = piece*1024 + t + 256e, e < 4 (any L).
+// VEC = 4: thread t owns x = piece*kRecPiece + 4(t + kRecThreads v) + e, v < kRecNV, e < 4
+// (needs L % 4 == 0 and aligned T); VEC = 1: x = piece*kRecPiece + t + kRecThreads i,
+// i < kRecV (any L).  Either way each load instruction of a block reads consecutive bytes.
 template <int VEC>
-__device__ __forceinline__ int64_t rec_x(int64_t q, int e) {
-  return VEC == 4 ? q * kRecPiece + int64_t(threadIdx.x) * 4 + e
-                  : q * kRecPiece + threadIdx.x + int64_t(kRecThreads) * e;
+__device__ __forceinline__ int64_t rec_x(int64_t q, int i) {
+  return VEC == 4 ? q * kRecPiece + (int64_t(threadIdx.x) + int64_t(kRecThreads) * (i / 4)) * 4 + i % 4
+                  : q * kRecPiece + threadIdx.x + int64_t(kRecThreads) * i;
 }
 
 template <int VEC>
-__device__ __forceinline__ void rec_load(const float *__restrict__ row, int64_t q, int64_t L, float (&v)[4]) {
+__device__ __forceinline__ void rec_load(const float *__restrict__ row, int64_t q, int64_t L,
+                                         float (&v)[kRecV]) {
   if constexpr (VEC == 4) {
-    const int64_t x = rec_x<4>(q, 0);
-    if (x < L) {
-      const v4f t = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(row + x));
-      v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-    } else {
-      v[0] = v[1] = v[2] = v[3] = 0.f;
+#pragma unroll
+    for (int u = 0; u < kRecNV; ++u) {
+      const int64_t x = rec_x<4>(q, 4 * u);
+      if (x < L) {
+        const v4f t = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(row + x));
+        v[4 * u] = t.x; v[4 * u + 1] = t.y; v[4 * u + 2] = t.z; v[4 * u + 3] = t.w;
+      } else {
+        v[4 * u] = v[4 * u + 1] = v[4 * u + 2] = v[4 * u + 3] = 0.f;
+      }
     }
   } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t x = rec_x<1>(q, e);
-      v[e] = x < L ? __builtin_nontemporal_load(row + x) : 0.f;
+    for (int i = 0; i < kRecV; ++i) {
+      const int64_t x = rec_x<1>(q, i);
+      v[i] = x < L ? __builtin_nontemporal_load(row + x) : 0.f;
     }
   }
 }
@@ -87,21 +95,21 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
   __syncthreads();
   const int nr = nrows;
 
-  float acc[ELL][4];
+  float acc[ELL][kRecV];
 #pragma unroll
   for (int k = 0; k < ELL; ++k)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) acc[k][e] = 0.f;
+    for (int i = 0; i < kRecV; ++i) acc[k][i] = 0.f;
 
   // software pipeline: the loads of the next kRecUnroll rows are in flight while the
   // current ones are consumed
-  float va[kRecUnroll][4], vb[kRecUnroll][4];
-  auto issue = [&](int a0, float (&v)[kRecUnroll][4]) {
+  float va[kRecUnroll][kRecV], vb[kRecUnroll][kRecV];
+  auto issue = [&](int a0, float (&v)[kRecUnroll][kRecV]) {
 #pragma unroll
     for (int u = 0; u < kRecUnroll; ++u)
       if (a0 + u < nr) rec_load<VEC>(Tp + int64_t(rows[a0 + u]) * L, q, L, v[u]);
   };
-  auto consume = [&](int a0, const float (&v)[kRecUnroll][4]) {
+  auto consume = [&](int a0, const float (&v)[kRecUnroll][kRecV]) {
 #pragma unroll
     for (int u = 0; u < kRecUnroll; ++u)
       if (a0 + u < nr)
@@ -109,7 +117,7 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
       for (int k = 0; k < ELL; ++k) {
         const float r = rw[k][a0 + u];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[k][e] = fmaf(r, v[u][e], acc[k][e]);
+        for (int i = 0; i < kRecV; ++i) acc[k][i] = fmaf(r, v[u][i], acc[k][i]);
       }
   };
   if (nr > 0) issue(0, va);
@@ -124,27 +132,31 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
   double se = 0.0;
 #pragma unroll
   for (int k = 0; k < ELL; ++k) {
-    const int64_t x0 = rec_x<VEC>(q, 0);
-    const int64_t c0 = int64_t(k) * L + x0;
-    if (VEC == 4 && x0 < L && c0 + 3 < d) {  // whole float4 inside the gradient
-      if (ghat)
-        *reinterpret_cast<float4 *>(ghat + p * d + c0) = make_float4(acc[k][0], acc[k][1], acc[k][2], acc[k][3]);
-      if (partial) {
-        const float4 g = *reinterpret_cast<const float4 *>(gsum + c0);
-        const double e0 = double(acc[k][0]) - g.x, e1 = double(acc[k][1]) - g.y;
-        const double e2 = double(acc[k][2]) - g.z, e3 = double(acc[k][3]) - g.w;
-        se += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
-      }
-    } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t x = rec_x<VEC>(q, e);
-        const int64_t col = int64_t(k) * L + x;
-        if (x < L && col < d) {
-          if (ghat) ghat[p * d + col] = acc[k][e];
-          if (partial) {
-            const double diff = double(acc[k][e]) - double(gsum[col]);
-            se += diff * diff;
+    for (int u = 0; u < kRecNV; ++u) {
+      const int64_t x0 = rec_x<VEC>(q, 4 * u);
+      const int64_t c0 = int64_t(k) * L + x0;
+      if (VEC == 4 && x0 < L && c0 + 3 < d) {  // whole float4 inside the gradient
+        const float *a4 = &acc[k][4 * u];
+        if (ghat)
+          *reinterpret_cast<float4 *>(ghat + p * d + c0) = make_float4(a4[0], a4[1], a4[2], a4[3]);
+        if (partial) {
+          const float4 g = *reinterpret_cast<const float4 *>(gsum + c0);
+          const double e0 = double(a4[0]) - g.x, e1 = double(a4[1]) - g.y;
+          const double e2 = double(a4[2]) - g.z, e3 = double(a4[3]) - g.w;
+          se += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t x = rec_x<VEC>(q, 4 * u + e);
+          const int64_t col = int64_t(k) * L + x;
+          if (x < L && col < d) {
+            if (ghat) ghat[p * d + col] = acc[k][4 * u + e];
+            if (partial) {
+              const double diff = double(acc[k][4 * u + e]) - double(gsum[col]);
+              se += diff * diff;
+            }
           }
         }
       }

@@ -134,11 +134,12 @@ def test_workspace_sizes():
     assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 1) == 4 * 512 * 2 * 16384
     # general path: one residual per sample row and point
     assert gcx.gc_chunk_grads_workspace_size(50, 512, 16385, 2) == 4 * 2 * 50 * 512
-    # one fp64 partial per (pattern, 1024-wide piece of a block), none when a block has one piece
-    assert gcx.gc_reconstruct_workspace_size(10000, 50, 16384, 1) == 8 * 10000 * 16
-    assert gcx.gc_reconstruct_workspace_size(10, 50, 1024, 1) == 0
-    assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 4) == 0
-    assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 128
+    # one fp64 partial per (pattern, 4096-wide piece of a block), none when a block has one piece
+    assert gcx.gc_reconstruct_workspace_size(10000, 50, 16384, 1) == 8 * 10000 * 4
+    assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 1) == 0
+    assert gcx.gc_reconstruct_workspace_size(10, 50, 4097, 1) == 8 * 10 * 2
+    assert gcx.gc_reconstruct_workspace_size(10, 50, 16384, 4) == 0
+    assert gcx.gc_reconstruct_workspace_size(10, 100, 1 << 20, 8) == 8 * 10 * 32
     # direct estimate: fp32 mixing rows padded to 32 columns (256-byte rounded), then one fp64
     # error partial per (row, 128-column tile)
     assert gcx.gc_decode_direct_workspace_size(10000, 50, 16384, 1) == 4 * 10000 * 64 + 8 * 10000 * 128
