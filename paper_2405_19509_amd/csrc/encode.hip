@@ -16,6 +16,8 @@
 //   - block -> (slice, row range) is XCD-aware: blocks are dispatched
 //     round-robin over the 8 XCDs, and every block of a slice runs on the
 //     same XCD, so its L2 serves the repeated slice staging.
+// When the slice of every chunk does not fit in LDS (many chunks, ell >= 2, bf16 at
+// large N) the worker-group layout below takes over.
 #include "common.h"
 
 namespace gcx {
@@ -97,16 +99,12 @@ struct EncodeArgs {
 };
 
 // LDS layout: [ G slice : N*ell*W GT ][ psi : group ][ chunk : group*delta ][ coef : group*delta*ell ]
-// STAGE = false (the slice of every chunk does not fit in LDS): no slice in
-// LDS; the gradient values are read from global memory, where L2 holds the
-// slice for the block's many rows.
-template <typename GT, int VEC, bool STAGE>
+template <typename GT, int VEC>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   constexpr int W = kWave * VEC;
   extern __shared__ __align__(16) unsigned char lds[];
   GT *Gs = reinterpret_cast<GT *>(lds);
-  const size_t gbytes =
-      STAGE ? (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15) : size_t(0);
+  const size_t gbytes = (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
   int32_t *mpsi = reinterpret_cast<int32_t *>(lds + gbytes);
   int32_t *mchunk = mpsi + a.group_rows;
   float *mcoef = reinterpret_cast<float *>(mchunk + size_t(a.group_rows) * a.delta);
@@ -129,7 +127,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   // stage the slice: Gs[(c*ell + k)*W + w] = g_c[k*L + x0 + w] (zero past L or past d),
   // 16 bytes per load where the run lies inside the gradient (d, L and G aligned to it)
   const GT *G = reinterpret_cast<const GT *>(a.G);
-  const int nrow = STAGE ? a.N * a.ell : 0;
+  const int nrow = a.N * a.ell;
   constexpr int SV = 16 / sizeof(GT);
   using SVT = uint4;
   for (int e = threadIdx.x * SV; e < nrow * W; e += kEncThreads * SV) {
@@ -188,17 +186,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
         for (int k = 0; k < a.ell; ++k) {
           const float w = mcoef[e * stride_row + t * a.ell + k];
           float g[VEC];
-          if constexpr (STAGE) {
-            load_vec<GT, VEC>(Gs + (size_t(c) * a.ell + k) * W + lane * VEC, g);
-          } else {
-            const int64_t col = int64_t(k) * a.L + xl;
-            if (xl < a.L && col < a.d) {
-              load_vec<GT, VEC>(G + int64_t(c) * a.d + col, g);
-            } else {
-#pragma unroll
-              for (int q = 0; q < VEC; ++q) g[q] = 0.f;
-            }
-          }
+          load_vec<GT, VEC>(Gs + (size_t(c) * a.ell + k) * W + lane * VEC, g);
 #pragma unroll
           for (int q = 0; q < VEC; ++q) acc[q] = fmaf(w, g[q], acc[q]);
         }
@@ -208,89 +196,391 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   }
 }
 
-// Per-worker layout, for ell >= 2 or many chunks, where the W-wide slice of every chunk
-// no longer fits in LDS at W = 256 floats: a block owns one worker j, one WW-wide slice of x
-// (WW = 1024, 512 or 256 floats: the widest whose delta*ell slices fit in kEwLds) and a
-// range of patterns, and stages only the slices of j's own delta chunks.  Consecutive
-// blocks take the slices of one row, then the next worker (the next row in memory), then
-// the next pattern range, so the blocks in flight write whole consecutive rows of T.
-// A wave writes one WW-wide row piece per transmitting pattern.
-constexpr int kEwThreads = 256;
-constexpr size_t kEwLds = 64 * 1024;   // slice budget
-constexpr int64_t kEwPatterns = 100;   // patterns per block
+// Worker-group layout, for when the slice of every chunk does not fit in LDS at the
+// chosen width (many chunks, ell >= 2, bf16 at N = 200, ...).  A block owns one
+// W-wide slice of x, a group of J consecutive workers and a range of patterns.
+// It stages the slices of the union of the group's chunks (J + delta - 1 chunks
+// under the cyclic assignment, so J is sized for that), up to the LDS capacity;
+// chunks past the capacity, possible under other orders, are read through L2.
+// A wave computes one worker for PB patterns at once: each gradient value read
+// from LDS feeds PB accumulators.  The coefficients of the PB rows arrive as one
+// coalesced load per 16 terms (lane 16*pb + i holds term tk0 + i of pattern pb)
+// and are broadcast with readlane; the LDS offset of each term's slice comes from
+// a per-group table the same way.  The blocks of a slice run back to back on one
+// XCD, so its L2 serves the groups' overlapping chunk slices.
+constexpr int kGrpThreads = 512;
+constexpr int kGrpWaves = kGrpThreads / kWave;
+constexpr size_t kGrpLds = 72 * 1024;  // per block: two blocks per CU
+static_assert(kGrpLds <= size_t(9) * 512 * 16, "one staging pass covers the slice budget");
+constexpr int kGrpTerms = 16;          // terms per coefficient load
+constexpr int kGrpStage = 9;           // 16-byte staging loads per thread: the whole slice
+constexpr int kGrpSkip = INT32_MIN;    // a padded order slot: no term
 
-template <typename GT, int WW>
-__global__ __launch_bounds__(kEwThreads) void encode_worker_kernel(EncodeArgs a, int64_t P,
-                                                                   int nsl) {
-  constexpr int NV = WW / (4 * kWave);  // 16-byte pieces per lane
+// 16 bytes of G from src (positions x.. of block column col..), zero past L or past d
+__device__ __forceinline__ uint32_t pick16(const float *src, int v, bool ok) {
+  return ok ? __float_as_uint(src[v]) : 0u;
+}
+__device__ __forceinline__ uint4 load16_guarded(const float *src, int64_t x, int64_t col, int64_t L,
+                                                int64_t d) {
+  uint32_t r[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) r[v] = pick16(src, v, x + v < L && col + v < d);
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+__device__ __forceinline__ uint4 load16_guarded(const uint16_t *src, int64_t x, int64_t col, int64_t L,
+                                                int64_t d) {
+  uint32_t r[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const uint32_t lo = (x + 2 * v < L && col + 2 * v < d) ? src[2 * v] : 0u;
+    const uint32_t hi = (x + 2 * v + 1 < L && col + 2 * v + 1 < d) ? src[2 * v + 1] : 0u;
+    r[v] = lo | (hi << 16);
+  }
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
+struct GroupArgs {
+  int J;          // workers per group
+  int ngroups;
+  int64_t PR;     // patterns per block
+  int64_t npr;    // pattern ranges
+  int slots;      // chunk slices the block can stage
+  int64_t P;
+  int64_t nsr;    // slice ranges (a multiple of 8)
+  int64_t spb;    // slices per range
+};
+
+__device__ __forceinline__ int readlane_i(int v, int lane) {
+  return __builtin_amdgcn_readlane(v, lane);
+}
+__device__ __forceinline__ float readlane_f(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// LDS: [ G slices : slots*ell*W GT ][ code : J*delta int32 ][ slot chunk : slots int32 ][ map : N int32 ]
+// W = 64*VEC*NV: lane l owns x = x0 + (64u + l)*VEC + v for u < NV, v < VEC, so every
+// load and store instruction of a wave covers 64*VEC consecutive positions.
+template <typename GT, int VEC, int NV, int PB>
+__global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))) void encode_group_kernel(
+    EncodeArgs a, GroupArgs g) {
+  constexpr int W = kWave * VEC * NV;
+  static_assert(PB >= 1 && PB * kGrpTerms <= kWave, "PB rows of 16 terms fill at most one wave");
   extern __shared__ __align__(16) unsigned char lds[];
-  GT *Gs = reinterpret_cast<GT *>(lds);  // [delta*ell][WW]
+  GT *Gs = reinterpret_cast<GT *>(lds);
+  const size_t gbytes = (size_t(g.slots) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
+  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes);
+  int32_t *slotc = code + g.J * a.delta;
+  int32_t *map = slotc + g.slots;
+  __shared__ int nslot;
+
+  // block -> (slice range, unit = (group, pattern range)).  Blocks are dispatched
+  // round-robin over the 8 XCDs; XCD x takes ranges x, x + 8, ..., and the blocks of all
+  // units of one range run back to back there, so its L2 serves the groups' overlapping
+  // chunk slices.  A block walks its range slice by slice with its group's tables built once.
   const int64_t b = blockIdx.x;
-  const int s = int(b % nsl);
-  const int j = int((b / nsl) % a.m);
-  const int64_t g = b / (int64_t(nsl) * a.m);
-  const int64_t x0 = int64_t(s) * WW;
-  const int nk = a.delta * a.ell;
-  const GT *G = reinterpret_cast<const GT *>(a.G);
-  for (int e = threadIdx.x; e < nk * WW; e += kEwThreads) {
-    const int tk = e / WW, w = e % WW;
-    const int t = tk / a.ell, k = tk % a.ell;
-    const int c = a.order[int64_t(j) * a.delta + t];
-    const int64_t x = x0 + w, col = int64_t(k) * a.L + x;
-    Gs[e] = (c >= 0 && c < a.N && x < a.L && col < a.d) ? G[int64_t(c) * a.d + col] : GT(0);
+  const int64_t units = int64_t(g.ngroups) * g.npr;
+  const int64_t sr = (b & 7) + 8 * ((b >> 3) / units);
+  const int64_t unit = (b >> 3) % units;
+  const int64_t s_begin = sr * g.spb;
+  const int64_t s_end = s_begin + g.spb < a.nslices ? s_begin + g.spb : a.nslices;
+  if (s_begin >= s_end) return;  // the whole block: an empty range at the end
+  const int gi = int(unit % g.ngroups);
+  const int64_t pi = unit / g.ngroups;
+  const int j0 = gi * g.J;
+  const int nj = a.m - j0 < g.J ? a.m - j0 : g.J;
+  const int64_t p0 = pi * g.PR;
+  const int64_t p1 = p0 + g.PR < g.P ? p0 + g.PR : g.P;
+  const int dl = a.delta * a.ell;
+
+  // 1. which chunks the group uses, then slots in ascending chunk order
+  for (int c = threadIdx.x; c < a.N; c += kGrpThreads) map[c] = 0;
+  __syncthreads();
+  for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
+    const int c = a.order[int64_t(j0) * a.delta + e];  // rows j0.. of order are contiguous
+    if (c >= 0 && c < a.N) map[c] = 1;
   }
   __syncthreads();
+  if (threadIdx.x < kWave) {
+    int cnt = 0;
+    for (int base = 0; base < a.N; base += kWave) {
+      const int c = base + int(threadIdx.x);
+      const bool on = c < a.N && map[c] != 0;
+      const unsigned long long mask = __ballot(on);
+      if (on) {
+        const int s_ = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
+        map[c] = s_ < g.slots ? s_ : -1;
+        if (s_ < g.slots) slotc[s_] = c;
+      } else if (c < a.N) {
+        map[c] = -1;
+      }
+      cnt += __popcll(mask);
+    }
+    if (threadIdx.x == 0) nslot = cnt < g.slots ? cnt : g.slots;
+  }
+  __syncthreads();
+  // per (worker, position): LDS offset of the slice of block 0 (>= 0), or -1 - c
+  // for a chunk read through L2, or kGrpSkip for a padded slot
+  for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
+    const int c = a.order[int64_t(j0) * a.delta + e];
+    int v = kGrpSkip;
+    if (c >= 0 && c < a.N) v = map[c] >= 0 ? map[c] * a.ell * W : -1 - c;
+    code[e] = v;
+  }
+  // 2. staging of a slice: Gs[(s*ell + k)*W + w] = g_{slotc[s]}[k*L + x0 + w] (zero past L
+  // or d), 16 bytes per thread and step, all of it in registers first; where the compute
+  // leaves room (PREF) the next slice's loads are issued before the current slice is
+  // computed, else each slice is loaded and stored in turn
+  const GT *G = reinterpret_cast<const GT *>(a.G);
+  constexpr int SV = 16 / sizeof(GT);
+  const int total = nslot * a.ell * W;
+  uint4 buf[kGrpStage];
+  auto stage_load = [&](int64_t x0) {
+#pragma unroll
+    for (int u = 0; u < kGrpStage; ++u) {
+      int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
+      // recomputed per slice rather than kept live through the compute
+      asm volatile("" : "+v"(e));
+      buf[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (e < total) {
+        const int sk = e / W, w = e % W;
+        const int c = slotc[sk / a.ell], k = sk % a.ell;
+        const int64_t x = x0 + w;
+        const int64_t col = int64_t(k) * a.L + x;
+        const GT *src = G + int64_t(c) * a.d + col;
+        if (a.stage16 && x + SV <= a.L && col + SV <= a.d)
+          buf[u] = *reinterpret_cast<const uint4 *>(src);
+        else
+          buf[u] = load16_guarded(src, x, col, a.L, a.d);
+      }
+    }
+  };
+  auto stage_store = [&]() {
+#pragma unroll
+    for (int u = 0; u < kGrpStage; ++u) {
+      const int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
+      if (e < total) *reinterpret_cast<uint4 *>(Gs + e) = buf[u];
+    }
+  };
+  constexpr bool PREF = PB * NV * VEC <= 16;
+  if constexpr (PREF) stage_load(s_begin * W);
 
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int64_t p0 = g * kEwPatterns;
-  const int64_t p1 = p0 + kEwPatterns < P ? p0 + kEwPatterns : P;
-  for (int64_t p = p0 + wave; p < p1; p += kEwThreads / kWave) {
-    const int64_t r = p * a.m + j;
-    int np = a.psi[r];
-    np = np < 0 ? 0 : (np > a.delta ? a.delta : np);
-    if (np == 0) continue;  // a worker that has processed nothing transmits nothing
-    const float *co = a.Bc + r * nk;
-    float acc[NV][4];
+  // 3. items (pattern batch, worker), worker fastest: the waves write neighbouring rows
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+  const int lane = threadIdx.x % kWave;
+  for (int64_t slice = s_begin; slice < s_end; ++slice) {
+  const int64_t x0 = slice * W;
+  __syncthreads();  // tables built; the previous slice's terms all applied
+  if constexpr (!PREF) stage_load(x0);
+  stage_store();
+  __syncthreads();
+  if constexpr (PREF) {
+    if (slice + 1 < s_end) stage_load(x0 + W);
+  }
+  const int64_t nb = ceil_div(p1 - p0, PB);
+  const int64_t items = nb * nj;
+  const int tl = lane % kGrpTerms, pl = lane / kGrpTerms;  // this lane's term and pattern
+  for (int64_t it = wave; it < items; it += kGrpWaves) {
+    const int jb = int(it % nj);
+    const int j = j0 + jb;
+    const int64_t pb0 = p0 + (it / nj) * PB;
+    // term tk0 + (lane % 16) of pattern pb0 + lane / 16: its coefficient, and the LDS offset
+    // of its slice (staged) or -1 - (c*ell + k) (chunk c, block k, read through L2)
+    const float *brow = a.Bc + ((pb0 + pl) * a.m + j) * int64_t(dl);
+    auto term_info = [&](int tk0, float &cv, int &cd) {
+      const int tk = tk0 + tl;
+      cv = (pl < PB && pb0 + pl < p1 && tk < dl) ? brow[tk] : 0.f;
+      cd = kGrpSkip;
+      if (tk < dl) {
+        const int t = tk / a.ell, k = tk - t * a.ell;
+        const int c0 = code[jb * a.delta + t];
+        cd = c0 == kGrpSkip ? kGrpSkip : (c0 >= 0 ? c0 + k * W : c0 * a.ell - k + (a.ell - 1));
+      }
+    };
+    float cvn;
+    int cdn;
+    term_info(0, cvn, cdn);  // issued before psi is known
+    // term limits psi*ell per pattern of the batch (0 past the range)
+    int lim_l = 0;
+    if (lane < PB && pb0 + lane < p1) {
+      int v = a.psi[(pb0 + lane) * a.m + j];
+      lim_l = (v < 0 ? 0 : (v > a.delta ? a.delta : v)) * a.ell;
+    }
+    int lim[PB];
+    int tmax = 0;
 #pragma unroll
-    for (int i = 0; i < NV; ++i)
+    for (int q = 0; q < PB; ++q) {
+      lim[q] = readlane_i(lim_l, q);
+      tmax = lim[q] > tmax ? lim[q] : tmax;
+    }
+    if (tmax == 0) continue;  // every pattern of the batch: a straggler, nothing sent
+    float acc[PB][NV][VEC];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[i][q] = 0.f;
-    for (int tk = 0; tk < np * a.ell; ++tk) {  // positions in order, blocks within a position
-      const float w = co[tk];
-      const GT *src = Gs + size_t(tk) * WW + lane * 4;
+    for (int q = 0; q < PB; ++q)
 #pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        float gv[4];
-        load_vec<GT, 4>(src + i * 4 * kWave, gv);
+      for (int u = 0; u < NV; ++u)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) acc[i][q] = fmaf(w, gv[q], acc[i][q]);
+        for (int v = 0; v < VEC; ++v) acc[q][u][v] = 0.f;
+    for (int tk0 = 0; tk0 < tmax; tk0 += kGrpTerms) {
+      const float cv = cvn;
+      const int cd = cdn;
+      // the next 16 terms' coefficients and slice offsets load while these are applied
+      if (tk0 + kGrpTerms < tmax) term_info(tk0 + kGrpTerms, cvn, cdn);
+#pragma unroll
+      for (int i = 0; i < kGrpTerms; ++i) {
+        if (tk0 + i >= tmax) break;
+        const int ci = readlane_i(cd, i);
+        if (ci == kGrpSkip) continue;
+        float gv[NV][VEC];
+        if (ci >= 0) {
+#pragma unroll
+          for (int u = 0; u < NV; ++u) load_vec<GT, VEC>(Gs + ci + (u * kWave + lane) * VEC, gv[u]);
+        } else {
+          const int ck = -1 - ci, c = ck / a.ell, k = ck - c * a.ell;
+#pragma unroll
+          for (int u = 0; u < NV; ++u) {
+            const int64_t x = x0 + int64_t(u * kWave + lane) * VEC;
+            const int64_t col = int64_t(k) * a.L + x;
+#pragma unroll
+            for (int v = 0; v < VEC; ++v)
+              gv[u][v] = (x + v < a.L && col + v < a.d) ? to_f32<GT>(G[int64_t(c) * a.d + col + v]) : 0.f;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < PB; ++q) {
+          if (tk0 + i < lim[q]) {
+            const float w = readlane_f(cv, q * kGrpTerms + i);
+#pragma unroll
+            for (int u = 0; u < NV; ++u)
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) acc[q][u][v] = fmaf(w, gv[u][v], acc[q][u][v]);
+          }
+        }
       }
     }
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int64_t x = x0 + i * 4 * kWave + lane * 4;
-      if (x < a.L) store_vec<4>(a.T + r * a.L + x, acc[i]);
+    for (int q = 0; q < PB; ++q) {
+      if (lim[q] == 0) continue;
+      float *row = a.T + ((pb0 + q) * a.m + j) * a.L;
+#pragma unroll
+      for (int u = 0; u < NV; ++u) {
+        const int64_t x = x0 + int64_t(u * kWave + lane) * VEC;
+        if (x < a.L) store_vec<VEC>(row + x, acc[q][u]);
+      }
     }
   }
+  }  // slice
 }
 
-template <typename GT, int WW>
-int launch_encode_worker(const EncodeArgs &a, int64_t P, hipStream_t st) {
-  const int nsl = int(ceil_div(a.L, WW));
-  const int64_t blocks = int64_t(nsl) * a.m * ceil_div(P, kEwPatterns);
-  if (!grid_ok(blocks, kEwThreads)) return GC_EINVAL;
-  const size_t lds = size_t(a.delta) * a.ell * WW * sizeof(GT);
-  hipLaunchKernelGGL((encode_worker_kernel<GT, WW>), dim3(unsigned(blocks)), dim3(kEwThreads), lds,
-                     st, a, P, nsl);
+// Sizes of the worker-group layout for a slice width W: the group J (for the cyclic
+// union of J + delta - 1 chunks), the slice capacity, the patterns per block (staged bytes
+// at most an eighth of those written, where the patterns allow).  Returns the ratio of
+// staged to written bytes, or a negative value when the layout does not fit.
+double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, GroupArgs &g, size_t &lds) {
+  const int64_t sb = int64_t(a.ell) * W * int64_t(esize);  // one chunk's slices
+  const int64_t B = int64_t(kGrpLds) - 16;
+  const int64_t dm1 = a.delta - 1;
+  int64_t J = (B - 4 * int64_t(a.N) - (sb + 4) * dm1) / (sb + 4 + 4 * int64_t(a.delta));
+  if (J > a.m) J = a.m;
+  if (J < 1) J = 1;
+  g.ngroups = int(ceil_div(a.m, J));
+  J = ceil_div(a.m, g.ngroups);  // balanced groups
+  int64_t slots = (B - 4 * (J * a.delta + a.N)) / (sb + 4);
+  const int64_t most = J * a.delta < a.N ? J * a.delta : a.N;
+  if (slots > most) slots = most;
+  if (slots < 1) return -1.0;
+  const int pb = P >= 4 ? 4 : 2;
+  const int64_t uni = J + dm1 < slots ? J + dm1 : slots;
+  int64_t pr = ceil_div(8 * uni * sb, J * W * 4);
+  pr = ceil_div(pr < 1 ? 1 : pr, pb) * pb;
+  if (pr > P) pr = P;
+  g.J = int(J);
+  g.PR = pr;
+  g.npr = ceil_div(P, pr);
+  g.slots = int(slots);
+  g.P = P;
+  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + sizeof(int32_t) * size_t(J * a.delta + slots + a.N);
+  if (lds > kGrpLds) return -1.0;
+  return double(uni * sb) / double(J * pr * W * 4);
+}
+
+template <typename GT, int VEC, int NV, int PB>
+int launch_group(const EncodeArgs &a, const GroupArgs &g, size_t lds, hipStream_t st) {
+  const int64_t blocks = g.nsr * g.ngroups * g.npr;
+  if (!grid_ok(blocks, kGrpThreads)) return GC_EINVAL;
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_group_kernel<GT, VEC, NV, PB>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
+    return GC_ELAUNCH;
+  hipLaunchKernelGGL((encode_group_kernel<GT, VEC, NV, PB>), dim3(unsigned(blocks)), dim3(kGrpThreads),
+                     lds, st, a, g);
   return GC_OK;
 }
 
-template <typename GT, int VEC, bool STAGE>
+// Candidate slice widths, widest first: (VEC, NV) = (4,4), (4,2), (4,1), (2,1), (1,1), i.e.
+// rows of 4 KB down to 256 B per wave, as far as the row length and T's alignment allow.
+// The widest candidate that stages the cyclic union of its group's chunks is taken (measured
+// on MI355X, wider rows always won once the union fits; a union that spills to L2 reads
+// costs 2-10x), else the narrowest.
+constexpr int kGrpCand = 5;
+constexpr int kGrpVec[kGrpCand] = {4, 4, 4, 2, 1};
+constexpr int kGrpNv[kGrpCand] = {4, 2, 1, 1, 1};
+
+int pick_group(const EncodeArgs &a, int64_t P, int vec, size_t esize, GroupArgs &g, size_t &lds) {
+  int pick = -1;
+  for (int i = 0; i < kGrpCand; ++i) {
+    if (kGrpVec[i] > vec) continue;
+    GroupArgs gi{};
+    size_t li = 0;
+    if (plan_group(a, P, int64_t(kWave) * kGrpVec[i] * kGrpNv[i], esize, gi, li) < 0) continue;
+    g = gi;
+    lds = li;
+    pick = i;
+    const int64_t uni = int64_t(gi.J) + a.delta - 1 < a.N ? int64_t(gi.J) + a.delta - 1 : a.N;
+    if (gi.slots >= uni) break;
+  }
+  return pick;
+}
+
+template <typename GT, int VEC>
+int launch_encode_group(EncodeArgs a, int64_t P, hipStream_t st) {
+  GroupArgs g{};
+  size_t lds = 0;
+  const int c = pick_group(a, P, VEC, sizeof(GT), g, lds);
+  if (c < 0) return GC_EINVAL;
+  a.nslices = int(ceil_div(a.L, int64_t(kWave) * kGrpVec[c] * kGrpNv[c]));
+  // enough work units to fill the chip: fewer patterns per block while they are short
+  const int pb = P >= 4 ? 4 : 2;
+  const int64_t want = 128 * int64_t(cu_count());  // blocks: about 64 rounds of resident ones
+  while (a.nslices * g.ngroups * g.npr < want / 2 && g.PR > pb) {
+    g.PR = ceil_div(g.PR / 2, pb) * pb;
+    g.npr = ceil_div(P, g.PR);
+  }
+  // slice ranges: a multiple of 8 (one share per XCD), about `want` blocks in all
+  const int64_t units = int64_t(g.ngroups) * g.npr;
+  int64_t nsr = ceil_div(ceil_div(want, units), 8) * 8;
+  if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
+  g.spb = ceil_div(a.nslices, nsr);
+  g.nsr = ceil_div(ceil_div(a.nslices, g.spb), 8) * 8;
+  const bool pb4 = P >= 4;
+  if constexpr (VEC == 4) {
+    if (c == 0)
+      return pb4 ? launch_group<GT, 4, 4, 4>(a, g, lds, st) : launch_group<GT, 4, 4, 2>(a, g, lds, st);
+    if (c == 1)
+      return pb4 ? launch_group<GT, 4, 2, 4>(a, g, lds, st) : launch_group<GT, 4, 2, 2>(a, g, lds, st);
+    if (c == 2)
+      return pb4 ? launch_group<GT, 4, 1, 4>(a, g, lds, st) : launch_group<GT, 4, 1, 2>(a, g, lds, st);
+  }
+  if constexpr (VEC >= 2) {
+    if (c == 3)
+      return pb4 ? launch_group<GT, 2, 1, 4>(a, g, lds, st) : launch_group<GT, 2, 1, 2>(a, g, lds, st);
+  }
+  return pb4 ? launch_group<GT, 1, 1, 4>(a, g, lds, st) : launch_group<GT, 1, 1, 2>(a, g, lds, st);
+}
+
+template <typename GT, int VEC>
 int launch_encode(EncodeArgs a, hipStream_t st) {
   constexpr int W = kWave * VEC;
   a.nslices = int(ceil_div(a.L, W));
-  const size_t gbytes =
-      STAGE ? (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15) : size_t(0);
+  const size_t gbytes = (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
   const size_t per_row = sizeof(int32_t) * (1 + a.delta) + sizeof(float) * a.delta * a.ell;
   int group = int(kEncMetaLds / per_row);
   if (group > kEncMaxGroup) group = kEncMaxGroup;
@@ -299,30 +589,28 @@ int launch_encode(EncodeArgs a, hipStream_t st) {
   // at most kEncRowsPerBlock rows per block, and a grid that is a whole number of rounds of
   // the blocks the chip holds at once (two per CU), so no round runs partly empty
   const int64_t conc = 2 * int64_t(cu_count());
-  int64_t g = a.nslices, h = conc;
-  while (h) { const int64_t t = g % h; g = h; h = t; }
-  const int64_t step = conc / g;  // row blocks per round of the grid
+  int64_t gg = a.nslices, h = conc;
+  while (h) { const int64_t t = gg % h; gg = h; h = t; }
+  const int64_t step = conc / gg;  // row blocks per round of the grid
   const int64_t rblocks = ceil_div(ceil_div(a.rows, kEncRowsPerBlock), step) * step;
   a.rows_per_block = ceil_div(a.rows, rblocks);
   const int64_t blocks = rblocks * a.nslices;
   if (!grid_ok(blocks, kEncThreads)) return GC_EINVAL;
   const size_t lds = gbytes + per_row * group;
-  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_kernel<GT, VEC, STAGE>),
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_kernel<GT, VEC>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
     return GC_ELAUNCH;
-  hipLaunchKernelGGL((encode_kernel<GT, VEC, STAGE>), dim3(unsigned(blocks)), dim3(kEncThreads), lds,
-                     st, a);
+  hipLaunchKernelGGL((encode_kernel<GT, VEC>), dim3(unsigned(blocks)), dim3(kEncThreads), lds, st, a);
   return GC_OK;
 }
 
 template <typename GT>
-int dispatch_encode(const EncodeArgs &a, int vec, bool stage, hipStream_t st) {
-  if (stage) {
-    return vec == 4 ? launch_encode<GT, 4, true>(a, st)
-                    : (vec == 2 ? launch_encode<GT, 2, true>(a, st) : launch_encode<GT, 1, true>(a, st));
-  }
-  return vec == 4 ? launch_encode<GT, 4, false>(a, st)
-                  : (vec == 2 ? launch_encode<GT, 2, false>(a, st) : launch_encode<GT, 1, false>(a, st));
+int dispatch_encode(const EncodeArgs &a, int64_t P, int vec, bool all_chunks, hipStream_t st) {
+  if (all_chunks)
+    return vec == 4 ? launch_encode<GT, 4>(a, st)
+                    : (vec == 2 ? launch_encode<GT, 2>(a, st) : launch_encode<GT, 1>(a, st));
+  return vec == 4 ? launch_encode_group<GT, 4>(a, P, st)
+                  : (vec == 2 ? launch_encode_group<GT, 2>(a, P, st) : launch_encode_group<GT, 1>(a, P, st));
 }
 
 }  // namespace
@@ -352,50 +640,17 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
   a.delta = delta;
   a.ell = ell;
   a.T = T;
-  // widest vector the row length and the alignment of T allow; stage the
-  // slice of every chunk in LDS when it fits, else read G through L2
+  // widest vector the row length and the alignment of T allow; the all-chunk layout
+  // when the slice of every chunk fits in LDS at that width, else the worker groups
   const size_t esize = g_dtype == GC_F32 ? 4 : 2;
   const uintptr_t ta = reinterpret_cast<uintptr_t>(T), ga = reinterpret_cast<uintptr_t>(G);
   const int64_t sv = int64_t(16 / esize);
   a.stage16 = d % sv == 0 && a.L % sv == 0 && (ga & 15) == 0;
-  int vec = (a.L % 4 == 0 && (ta & 15) == 0) ? 4 : ((a.L % 2 == 0 && (ta & 7) == 0) ? 2 : 1);
-  int svec = vec;
-  while (svec > 1 && size_t(N) * ell * kWave * svec * esize > kEncSliceLds) svec >>= 1;
-  const bool stage = size_t(N) * ell * kWave * svec * esize <= kEncSliceLds;
-  if (stage) {
-    vec = svec;
-  } else {
-    // direct vector loads of G need d and the base to be multiples of the vector
-    while (vec > 1 && (d % vec != 0 || (ga & (size_t(vec) * esize - 1)) != 0)) vec >>= 1;
-  }
+  const int vec = (a.L % 4 == 0 && (ta & 15) == 0) ? 4 : ((a.L % 2 == 0 && (ta & 7) == 0) ? 2 : 1);
+  const bool all_chunks = size_t(N) * ell * kWave * vec * esize <= kEncSliceLds;
   (void)hipGetLastError();
-  // when the all-chunk slice cannot stay 256 wide, the per-worker layout at the widest slice
-  // (1024, 512 or 256) that fits, given 16-byte rows of T and enough patterns per block to
-  // repay the staging of each worker's slices: its staged bytes, ceil(P/100)*delta*ell*esize
-  // per row position, at most half of the 4*P bytes of T there (with very few patterns the
-  // all-chunk layout stages every chunk's slice once for all the rows)
-  const bool ew_pays = 2 * ceil_div(P, kEwPatterns) * delta * ell * int64_t(esize) <= 4 * P;
-  if (a.L % 4 == 0 && (ta & 15) == 0 && (!stage || svec < 4) && ew_pays) {
-    const size_t per = size_t(delta) * ell * esize;  // LDS bytes per slice position
-    int ww = 0;
-    for (int w = 1024; w >= 256 && !ww; w >>= 1)
-      if (per * w <= kEwLds) ww = w;
-    if (ww) {
-      int st;
-      if (g_dtype == GC_F32)
-        st = ww == 1024 ? launch_encode_worker<float, 1024>(a, P, stream)
-             : ww == 512 ? launch_encode_worker<float, 512>(a, P, stream)
-                         : launch_encode_worker<float, 256>(a, P, stream);
-      else
-        st = ww == 1024 ? launch_encode_worker<uint16_t, 1024>(a, P, stream)
-             : ww == 512 ? launch_encode_worker<uint16_t, 512>(a, P, stream)
-                         : launch_encode_worker<uint16_t, 256>(a, P, stream);
-      if (st != GC_OK) return st;
-      return launch_status();
-    }
-  }
-  const int st = g_dtype == GC_F32 ? dispatch_encode<float>(a, vec, stage, stream)
-                                   : dispatch_encode<uint16_t>(a, vec, stage, stream);
+  const int st = g_dtype == GC_F32 ? dispatch_encode<float>(a, P, vec, all_chunks, stream)
+                                   : dispatch_encode<uint16_t>(a, P, vec, all_chunks, stream);
   if (st != GC_OK) return st;
   return launch_status();
 }

@@ -234,6 +234,31 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     assert (host(sq2) == sqerr).all()
 
 
+# worker-group encode layout: many chunks per slice, so the all-chunk layout does not fit;
+# odd L (one float per lane), padding (ell does not divide d), bf16, 1 to 7 patterns per call
+GROUP_CASES = [
+    (Workload(name="group_m130_d3002", N=130, m=130, s=3, d=3002, P=7, ells=(3,), pattern="uniform"), 3, 1),
+    (Workload(name="group_m130_d3002", N=130, m=130, s=3, d=3002, P=7, ells=(3,), pattern="uniform"), 3, 7),
+    (Workload(name="group_m200_d4001_bf16", N=200, m=200, s=5, d=4001, P=3, ells=(4,), g_dtype="bf16",
+              pattern="uniform"), 4, 3),
+    (Workload(name="group_m120_d8192", N=120, m=120, s=9, d=8192, P=5, ells=(2,), pattern="uniform"), 2, 5),
+]
+
+
+@pytest.mark.parametrize("wl,ell,count", GROUP_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in GROUP_CASES])
+def test_encode_worker_groups(wl, ell, count):
+    O, order, _, _ = tables(wl)
+    psi = patterns(wl, count)
+    R = gen.shared_R(wl.m, ell)
+    Bc32 = R_.coefficients(O, psi, R)[0].astype(np.float32)
+    G = given_G(wl)
+    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32)))
+    T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, wl.g_dtype), ell)
+    sent = psi > 0
+    bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
+
+
 def _uneven_assignment(seed=5):
     """9 chunks over 6 workers, 2 or 3 holders per chunk, loads 3 to 5, orders shuffled."""
     N, m = 9, 6
