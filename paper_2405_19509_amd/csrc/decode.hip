@@ -222,11 +222,16 @@ template <int ELL>
 struct DecodeLayout {
   static constexpr int NF = ELL * (ELL + 1) / 2;  // packed lower triangle
   // words (4 bytes) of the block-shared part and of one wave's region
-  // tables [gamma][N] x 2, loads [m], Rs [ELL][m] + a zero for the sentinel worker m,
-  // and with Bc the order table [m][delta] (entries past the chunks: the sentinel chunk N)
+  // at ell = 1 with Bc the squares R_j^2 in fp64 [m + 1] (exact: fp32 squared fits fp64);
+  // holder table [gamma][N] (worker | position << 16), loads [m], Rs [ELL][m] + a zero
+  // for the sentinel worker m, and with Bc the order table [m][delta] as int16 (entries
+  // past the chunks: the sentinel chunk N)
+  __host__ __device__ static int64_t r2_words(int m, bool bc) {
+    return (ELL == 1 && bc) ? 2 * int64_t(m + 1) : 0;
+  }
   __host__ __device__ static int64_t shared_words(int N, int m, int gamma, int delta, bool bc) {
-    const int64_t ord = bc ? int64_t(m) * delta : 0;
-    return (2 * int64_t(gamma) * N + m + int64_t(ELL) * m + 1 + ord + 3) & ~int64_t(3);
+    const int64_t ord = bc ? (int64_t(m) * delta + 1) / 2 : 0;
+    return (r2_words(m, bc) + int64_t(gamma) * N + m + int64_t(ELL) * m + 1 + ord + 3) & ~int64_t(3);
   }
   // F [N + 1][NF] doubles (row N: the sentinel chunk, zero), covS [N + 1], sel [N][ELL]
   // (ell > 1), psi [m + 1] (entry m: the sentinel worker)
@@ -250,20 +255,19 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
   using Lay = DecodeLayout<ELL>;
   constexpr int NF = Lay::NF;
   extern __shared__ __align__(16) int32_t sh[];
-  int32_t *holdT = sh;                           // [gamma][N]
-  int32_t *hposT = holdT + int64_t(gamma) * N;   // [gamma][N]
-  int32_t *loads = hposT + int64_t(gamma) * N;   // [m]
-  float *Rs = reinterpret_cast<float *>(loads + m);  // [ELL][m] + 1
-  int32_t *ordS = reinterpret_cast<int32_t *>(Rs + ELL * m + 1);  // [m][delta] (with Bc)
   const bool want_bc = Bc != nullptr;
+  double *R2s = reinterpret_cast<double *>(sh);  // [m + 1] (ell = 1 with Bc)
+  int32_t *hjt = sh + Lay::r2_words(m, want_bc);  // [gamma][N]: j | t << 16
+  int32_t *loads = hjt + int64_t(gamma) * N;     // [m]
+  float *Rs = reinterpret_cast<float *>(loads + m);  // [ELL][m] + 1
+  int16_t *ordS = reinterpret_cast<int16_t *>(Rs + ELL * m + 1);  // [m][delta] (with Bc)
   // table entries outside [0, m) x [0, delta) point at the sentinel worker m, whose psi
   // entry is -1 (never past any position) and whose weight is 0
   for (int e = threadIdx.x; e < N * gamma; e += blockDim.x) {
     const int i = e / gamma, u = e % gamma;
     const int j = holder[e], t = hpos[e];
     const bool ok = j >= 0 && j < m && t >= 0 && t < delta;
-    holdT[int64_t(u) * N + i] = ok ? j : m;
-    hposT[int64_t(u) * N + i] = ok ? t : 0;
+    hjt[int64_t(u) * N + i] = ok ? (j | (t << 16)) : m;
   }
   for (int j = threadIdx.x; j < m; j += blockDim.x) {
     int load = 0;
@@ -276,9 +280,14 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
   if (want_bc) {
     for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
     if (threadIdx.x == 0) Rs[ELL * m] = 0.f;
+    if (ELL == 1)
+      for (int j = threadIdx.x; j <= m; j += blockDim.x) {
+        const double x = j < m ? double(R[j]) : 0.0;
+        R2s[j] = x * x;
+      }
     for (int e = threadIdx.x; e < m * delta; e += blockDim.x) {
       const int c = order[e];
-      ordS[e] = (c >= 0 && c < N) ? c : N;
+      ordS[e] = int16_t((c >= 0 && c < N) ? c : N);
     }
   }
   __syncthreads();  // the only block barrier; every thread reaches it
@@ -320,14 +329,23 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
     for (int i = lane; i < N; i += kWave) {
       int Delta = 0;
       double ss = 0.0;  // ell = 1: sum of R_j^2 over the members, in holder order
+      if (ELL == 1 && want_bc) {
+        // branch-free, every load unconditional (the sentinel worker m has psi -1 and
+        // weight 0), so the unrolled holders' LDS reads overlap
 #pragma unroll 4
-      for (int u = 0; u < gamma; ++u) {  // branch-free: non-members add 0
-        const int j = holdT[u * N + i], t = hposT[u * N + i];
-        const bool member = pss[j] > t;
-        Delta += member ? 1 : 0;
-        if (ELL == 1 && want_bc) {
-          const double x = Rs[j];
-          ss += member ? x * x : 0.0;
+        for (int u = 0; u < gamma; ++u) {
+          const int jt = hjt[u * N + i], j = jt & 0xffff, t = jt >> 16;
+          const int pv = pss[j];
+          const double x2 = R2s[j];
+          const bool member = pv > t;
+          Delta += member ? 1 : 0;
+          ss += member ? x2 : 0.0;
+        }
+      } else {
+#pragma unroll 4
+        for (int u = 0; u < gamma; ++u) {
+          const int jt = hjt[u * N + i], j = jt & 0xffff, t = jt >> 16;
+          Delta += pss[j] > t ? 1 : 0;
         }
       }
       if (cov != nullptr) cov[p * N + i] = Delta;
@@ -351,7 +369,7 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
 #pragma unroll
           for (int b = 0; b < ELL; ++b) M[a][b] = 0.0;
         for (int u = 0; u < gamma; ++u) {
-          const int j = holdT[u * N + i], t = hposT[u * N + i];
+          const int jt = hjt[u * N + i], j = jt & 0xffff, t = jt >> 16;
           if (pss[j] > t) {
             double x[ELL];
 #pragma unroll
@@ -373,7 +391,7 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
         for (int a = 0; a < ELL; ++a) selj[a] = -1;
         int cnt = 0;
         for (int u = 0; u < gamma; ++u) {
-          const int j = holdT[u * N + i], t = hposT[u * N + i];
+          const int jt = hjt[u * N + i], j = jt & 0xffff, t = jt >> 16;
           if (pss[j] > t) {
 #pragma unroll
             for (int a = 0; a < ELL; ++a)
@@ -425,17 +443,56 @@ __global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_til
       // four consecutive rows per lane, one 16-byte store
       int j4 = (4 * lane) / delta, t4 = (4 * lane) % delta;
       const int j4_step = (4 * kWave) / delta, t4_step = (4 * kWave) % delta;
-      for (int e0 = 4 * lane; e0 < nrow; e0 += 4 * kWave) {
+      for (int e0 = 4 * lane; (delta & 3) == 0 && e0 < nrow; e0 += 4 * kWave) {
+        // delta a multiple of 4: the four rows are positions t4 .. t4 + 3 of one worker
+        double f[4];  // zero for the sentinel chunk, Delta = 0, invalid
+#pragma unroll
+        for (int q = 0; q < 4; ++q) f[q] = F[ordS[e0 + q]];
+        const int pv = pss[j4];
+        const double r = Rs[j4];
         float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float v = float(r * f[q]);
+          o[q] = (pv > t4 + q && f[q] != 0.0) ? v : 0.f;
+        }
+        *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
+        j4 += j4_step;
+        t4 += t4_step;
+        if (t4 >= delta) {
+          t4 -= delta;
+          ++j4;
+        }
+      }
+      for (int e0 = 4 * lane; (delta & 3) != 0 && e0 < nrow; e0 += 4 * kWave) {
+        // the four rows' (worker, position), then every LDS read, then the selects: no
+        // branches, so the reads of the four rows overlap
+        int jq[4], tq[4], cq[4];
         int jj = j4, tt = t4;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const double f = F[ordS[e0 + q]];  // zero for the sentinel chunk, Delta = 0, invalid
-          o[q] = (pss[jj] > tt && f != 0.0) ? float(double(Rs[jj]) * f) : 0.f;
+          jq[q] = jj;
+          tq[q] = tt;
+          cq[q] = ordS[e0 + q];
           if (++tt == delta) {
             tt = 0;
             ++jj;
           }
+        }
+        double f[4];  // zero for the sentinel chunk, Delta = 0, invalid
+        int pv[4];
+        float r[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          f[q] = F[cq[q]];
+          pv[q] = pss[jq[q]];
+          r[q] = Rs[jq[q]];
+        }
+        float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float v = float(double(r[q]) * f[q]);
+          o[q] = (pv[q] > tq[q] && f[q] != 0.0) ? v : 0.f;
         }
         *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
         j4 += j4_step;
