@@ -247,7 +247,8 @@ template <int ELL>
 constexpr int decode_tiled_max_waves() { return ELL <= 4 ? 16 : 4; }
 
 template <int ELL>
-__global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64) void decode_tiled_kernel(
+__global__ __launch_bounds__(decode_tiled_max_waves<ELL>() * 64)
+__attribute__((amdgpu_waves_per_eu(ELL <= 2 ? 8 : 1))) void decode_tiled_kernel(
     const int32_t *__restrict__ psi, int64_t P, int N, int m, const int32_t *__restrict__ order,
     int delta, const int32_t *__restrict__ holder, const int32_t *__restrict__ hpos, int gamma,
     const float *__restrict__ R, int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
