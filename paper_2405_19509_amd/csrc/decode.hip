@@ -602,7 +602,9 @@ bool launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *o
       best_w = w;
     }
   }
-  if (best_total >= 8) {  // else the one-phase kernel, which needs no LDS per wave
+  // else the one-phase kernel, which needs no LDS per wave (the two-phase kernel's order
+  // table holds chunk indices as int16)
+  if (best_total >= 8 && N < 32768) {
     const size_t lds = shared + best_w * per_wave;
     const int64_t want = ceil_div(P, best_w);
     const int64_t resident = int64_t(best_total / best_w) * cu_count();

@@ -248,6 +248,7 @@ struct GroupArgs {
   int64_t P;
   int64_t nsr;    // slice ranges (a multiple of 8)
   int64_t spb;    // slices per range
+  int dense;      // 1: chunk -> slot map over all N chunks; 0 (J = 1): slot t = position t
 };
 
 __device__ __forceinline__ int readlane_i(int v, int lane) {
@@ -270,7 +271,7 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))
   const size_t gbytes = (size_t(g.slots) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
   int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes);
   int32_t *slotc = code + g.J * a.delta;
-  int32_t *map = slotc + g.slots;
+  int32_t *map = slotc + g.slots;  // [N] (dense)
   __shared__ int nslot;
 
   // block -> (slice range, unit = (group, pattern range)).  Blocks are dispatched
@@ -293,38 +294,50 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))
   const int dl = a.delta * a.ell;
 
   // 1. which chunks the group uses, then slots in ascending chunk order
-  for (int c = threadIdx.x; c < a.N; c += kGrpThreads) map[c] = 0;
-  __syncthreads();
-  for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
-    const int c = a.order[int64_t(j0) * a.delta + e];  // rows j0.. of order are contiguous
-    if (c >= 0 && c < a.N) map[c] = 1;
-  }
-  __syncthreads();
-  if (threadIdx.x < kWave) {
-    int cnt = 0;
-    for (int base = 0; base < a.N; base += kWave) {
-      const int c = base + int(threadIdx.x);
-      const bool on = c < a.N && map[c] != 0;
-      const unsigned long long mask = __ballot(on);
-      if (on) {
-        const int s_ = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
-        map[c] = s_ < g.slots ? s_ : -1;
-        if (s_ < g.slots) slotc[s_] = c;
-      } else if (c < a.N) {
-        map[c] = -1;
-      }
-      cnt += __popcll(mask);
+  if (g.dense) {
+    for (int c = threadIdx.x; c < a.N; c += kGrpThreads) map[c] = 0;
+    __syncthreads();
+    for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
+      const int c = a.order[int64_t(j0) * a.delta + e];  // rows j0.. of order are contiguous
+      if (c >= 0 && c < a.N) map[c] = 1;
     }
-    if (threadIdx.x == 0) nslot = cnt < g.slots ? cnt : g.slots;
-  }
-  __syncthreads();
-  // per (worker, position): LDS offset of the slice of block 0 (>= 0), or -1 - c
-  // for a chunk read through L2, or kGrpSkip for a padded slot
-  for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
-    const int c = a.order[int64_t(j0) * a.delta + e];
-    int v = kGrpSkip;
-    if (c >= 0 && c < a.N) v = map[c] >= 0 ? map[c] * a.ell * W : -1 - c;
-    code[e] = v;
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+      int cnt = 0;
+      for (int base = 0; base < a.N; base += kWave) {
+        const int c = base + int(threadIdx.x);
+        const bool on = c < a.N && map[c] != 0;
+        const unsigned long long mask = __ballot(on);
+        if (on) {
+          const int s_ = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
+          map[c] = s_ < g.slots ? s_ : -1;
+          if (s_ < g.slots) slotc[s_] = c;
+        } else if (c < a.N) {
+          map[c] = -1;
+        }
+        cnt += __popcll(mask);
+      }
+      if (threadIdx.x == 0) nslot = cnt < g.slots ? cnt : g.slots;
+    }
+    __syncthreads();
+    // per (worker, position): LDS offset of the slice of block 0 (>= 0), or -1 - c
+    // for a chunk read through L2, or kGrpSkip for a padded slot
+    for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
+      const int c = a.order[int64_t(j0) * a.delta + e];
+      int v = kGrpSkip;
+      if (c >= 0 && c < a.N) v = map[c] >= 0 ? map[c] * a.ell * W : -1 - c;
+      code[e] = v;
+    }
+  } else {
+    // one worker (a worker's chunks are distinct): slot t holds position t
+    for (int t = threadIdx.x; t < a.delta; t += kGrpThreads) {
+      const int c = a.order[int64_t(j0) * a.delta + t];
+      const bool ok = c >= 0 && c < a.N;
+      if (t < g.slots) slotc[t] = ok ? c : 0;  // a padded slot stages chunk 0, never read
+      code[t] = !ok ? kGrpSkip : (t < g.slots ? t * a.ell * W : -1 - c);
+    }
+    if (threadIdx.x == 0) nslot = a.delta < g.slots ? a.delta : g.slots;
+    __syncthreads();
   }
   // 2. staging of a slice: Gs[(s*ell + k)*W + w] = g_{slotc[s]}[k*L + x0 + w] (zero past L
   // or d), 16 bytes per thread and step, all of it in registers first; where the compute
@@ -479,12 +492,16 @@ double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, Group
   const int64_t sb = int64_t(a.ell) * W * int64_t(esize);  // one chunk's slices
   const int64_t B = int64_t(kGrpLds) - 16;
   const int64_t dm1 = a.delta - 1;
-  int64_t J = (B - 4 * int64_t(a.N) - (sb + 4) * dm1) / (sb + 4 + 4 * int64_t(a.delta));
+  // the dense chunk map needs 4N bytes; past a quarter of the budget, single-worker
+  // groups, whose slots need no map
+  g.dense = 4 * int64_t(a.N) <= B / 4 ? 1 : 0;
+  const int64_t mapw = g.dense ? a.N : 0;
+  int64_t J = g.dense ? (B - 4 * mapw - (sb + 4) * dm1) / (sb + 4 + 4 * int64_t(a.delta)) : 1;
   if (J > a.m) J = a.m;
   if (J < 1) J = 1;
   g.ngroups = int(ceil_div(a.m, J));
   J = ceil_div(a.m, g.ngroups);  // balanced groups
-  int64_t slots = (B - 4 * (J * a.delta + a.N)) / (sb + 4);
+  int64_t slots = (B - 4 * (J * a.delta + mapw)) / (sb + 4);
   const int64_t most = J * a.delta < a.N ? J * a.delta : a.N;
   if (slots > most) slots = most;
   if (slots < 1) return -1.0;
@@ -498,7 +515,7 @@ double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, Group
   g.npr = ceil_div(P, pr);
   g.slots = int(slots);
   g.P = P;
-  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + sizeof(int32_t) * size_t(J * a.delta + slots + a.N);
+  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + sizeof(int32_t) * size_t(J * a.delta + slots + mapw);
   if (lds > kGrpLds) return -1.0;
   return double(uni * sb) / double(J * pr * W * 4);
 }

@@ -259,6 +259,25 @@ def test_encode_worker_groups(wl, ell, count):
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
 
 
+@pytest.mark.parametrize("ell,d", [(1, 512), (2, 513)])
+def test_encode_many_chunks(ell, d):
+    """5,000 chunks, 8 workers each holding 6 (one worker 4) of them in an explicit order:
+    more chunks than the per-group chunk map holds, so single-worker groups; random
+    coefficients (the encode is linear in them) against the oracle's encode."""
+    N, m, delta, P = 5000, 8, 6, 5
+    g = np.random.default_rng(21 + ell)
+    order = np.stack([g.choice(N, size=delta, replace=False) for _ in range(m)]).astype(np.int32)
+    order[3, 4:] = -1                                    # a worker with a shorter order
+    psi = g.integers(0, delta + 1, size=(P, m)).astype(np.int32)
+    psi[:, 3] = np.minimum(psi[:, 3], 4)
+    Bc = g.standard_normal((P, m, delta, ell)).astype(np.float32)
+    G = g.standard_normal((N, d)).astype(np.float32)
+    T = host(gcx.gc_encode(dev(G), dev(psi), dev(order), dev(Bc)))
+    T_ref, M, nterm = R_.encode_ref(Bc.astype(np.float64), psi, order, G.astype(np.float64), ell)
+    sent = psi > 0
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+
+
 def _uneven_assignment(seed=5):
     """9 chunks over 6 workers, 2 or 3 holders per chunk, loads 3 to 5, orders shuffled."""
     N, m = 9, 6
