@@ -252,11 +252,33 @@ def test_encode_worker_groups(wl, ell, count):
     R = gen.shared_R(wl.m, ell)
     Bc32 = R_.coefficients(O, psi, R)[0].astype(np.float32)
     G = given_G(wl)
-    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32)))
+    # rows of workers with psi = 0 transmit nothing and must stay untouched
+    Td = torch.full((len(psi), wl.m, -(-wl.d // ell)), float("nan"), device="cuda")
+    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32), T=Td))
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, wl.g_dtype), ell)
     sent = psi > 0
+    assert np.isnan(T[~sent]).all()
     bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
+
+
+@pytest.mark.parametrize("wl,ell", [(TINY, 2), (GROUP_CASES[3][0], 2)], ids=["all-chunk", "worker-group"])
+def test_encode_clamps_psi(wl, ell):
+    """psi outside [0, delta] is clamped, in both encode layouts: a negative count sends
+    nothing, a count past the load encodes the whole order."""
+    O, order, _, _ = tables(wl)
+    g = np.random.default_rng(31)
+    P = 6
+    psi = g.integers(-3, wl.delta + 4, size=(P, wl.m)).astype(np.int32)
+    Bc = g.standard_normal((P, wl.m, wl.delta, ell)).astype(np.float32)
+    G = given_G(wl)
+    Td = torch.full((P, wl.m, -(-wl.d // ell)), float("nan"), device="cuda")
+    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc), T=Td))
+    clamped = np.clip(psi, 0, wl.delta)
+    T_ref, M, nterm = R_.encode_ref(Bc.astype(np.float64), clamped, order, OP.widen(G, wl.g_dtype), ell)
+    sent = clamped > 0
+    assert np.isnan(T[~sent]).all()
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
 
 
 @pytest.mark.parametrize("ell,d", [(1, 512), (2, 513)])
