@@ -191,7 +191,10 @@ int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m, const 
  * held.  G [N][d] device in g_dtype; psi [P][m], order
  * [m][delta] int32 device; Bc [P][m][delta][ell] fp32 device (as from
  * gc_decode_coeffs); T [P][m][L] fp32 device.  fp32 accumulation.  psi is
- * clamped to [0, delta] and padded order slots are skipped.
+ * clamped to [0, delta] and padded order slots are skipped.  G must be finite:
+ * with 32 or more patterns per call and delta*ell >= 32 the sums run on the
+ * matrix cores, where a coefficient past a pattern's prefix enters as zero (and
+ * zero times a non-finite value is not zero).
  */
 int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_t *psi,
               const int32_t *order, const float *Bc, int64_t P, int32_t m, int32_t delta,

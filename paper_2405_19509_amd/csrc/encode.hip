@@ -63,6 +63,7 @@ __device__ __forceinline__ void load_vec(const GT *p, float (&v)[VEC]) {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 // T is written once and read back only by the combine: non-temporal stores
 // keep it from displacing the chunk-gradient slices in L2.
@@ -208,6 +209,11 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
 // and are broadcast with readlane; the LDS offset of each term's slice comes from
 // a per-group table the same way.  The blocks of a slice run back to back on one
 // XCD, so its L2 serves the groups' overlapping chunk slices.
+// With a full 32-pattern tile per call and delta*ell >= 32 terms per output (a dense
+// contraction [32 patterns][terms] x [terms][128 positions] per worker), a block whose
+// group's chunks are all staged runs its items on the matrix cores instead
+// (v_mfma_f32_32x32x2f32; coefficients past a pattern's prefix enter as zeros, so the
+// gradient values must be finite).
 constexpr int kGrpThreads = 512;
 constexpr int kGrpWaves = kGrpThreads / kWave;
 constexpr size_t kGrpLds = 72 * 1024;  // per block: two blocks per CU
@@ -258,137 +264,15 @@ __device__ __forceinline__ float readlane_f(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// LDS: [ G slices : slots*ell*W GT ][ code : J*delta int32 ][ slot chunk : slots int32 ][ map : N int32 ]
-// W = 64*VEC*NV: lane l owns x = x0 + (64u + l)*VEC + v for u < NV, v < VEC, so every
-// load and store instruction of a wave covers 64*VEC consecutive positions.
+// The items of one staged slice on the vector units: (pattern batch of PB, worker), worker
+// fastest, so the waves write neighbouring rows.
 template <typename GT, int VEC, int NV, int PB>
-__global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))) void encode_group_kernel(
-    EncodeArgs a, GroupArgs g) {
-  constexpr int W = kWave * VEC * NV;
-  static_assert(PB >= 1 && PB * kGrpTerms <= kWave, "PB rows of 16 terms fill at most one wave");
-  extern __shared__ __align__(16) unsigned char lds[];
-  GT *Gs = reinterpret_cast<GT *>(lds);
-  const size_t gbytes = (size_t(g.slots) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
-  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes);
-  int32_t *slotc = code + g.J * a.delta;
-  int32_t *map = slotc + g.slots;  // [N] (dense)
-  __shared__ int nslot;
-
-  // block -> (slice range, unit = (group, pattern range)).  Blocks are dispatched
-  // round-robin over the 8 XCDs; XCD x takes ranges x, x + 8, ..., and the blocks of all
-  // units of one range run back to back there, so its L2 serves the groups' overlapping
-  // chunk slices.  A block walks its range slice by slice with its group's tables built once.
-  const int64_t b = blockIdx.x;
-  const int64_t units = int64_t(g.ngroups) * g.npr;
-  const int64_t sr = (b & 7) + 8 * ((b >> 3) / units);
-  const int64_t unit = (b >> 3) % units;
-  const int64_t s_begin = sr * g.spb;
-  const int64_t s_end = s_begin + g.spb < a.nslices ? s_begin + g.spb : a.nslices;
-  if (s_begin >= s_end) return;  // the whole block: an empty range at the end
-  const int gi = int(unit % g.ngroups);
-  const int64_t pi = unit / g.ngroups;
-  const int j0 = gi * g.J;
-  const int nj = a.m - j0 < g.J ? a.m - j0 : g.J;
-  const int64_t p0 = pi * g.PR;
-  const int64_t p1 = p0 + g.PR < g.P ? p0 + g.PR : g.P;
+__device__ __forceinline__ void group_vector(const EncodeArgs &a, const GT *__restrict__ Gs,
+                                             const int32_t *__restrict__ code, int64_t x0, int j0, int nj,
+                                             int64_t p0, int64_t p1, int wave, int lane) {
   const int dl = a.delta * a.ell;
-
-  // 1. which chunks the group uses, then slots in ascending chunk order
-  if (g.dense) {
-    for (int c = threadIdx.x; c < a.N; c += kGrpThreads) map[c] = 0;
-    __syncthreads();
-    for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
-      const int c = a.order[int64_t(j0) * a.delta + e];  // rows j0.. of order are contiguous
-      if (c >= 0 && c < a.N) map[c] = 1;
-    }
-    __syncthreads();
-    if (threadIdx.x < kWave) {
-      int cnt = 0;
-      for (int base = 0; base < a.N; base += kWave) {
-        const int c = base + int(threadIdx.x);
-        const bool on = c < a.N && map[c] != 0;
-        const unsigned long long mask = __ballot(on);
-        if (on) {
-          const int s_ = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
-          map[c] = s_ < g.slots ? s_ : -1;
-          if (s_ < g.slots) slotc[s_] = c;
-        } else if (c < a.N) {
-          map[c] = -1;
-        }
-        cnt += __popcll(mask);
-      }
-      if (threadIdx.x == 0) nslot = cnt < g.slots ? cnt : g.slots;
-    }
-    __syncthreads();
-    // per (worker, position): LDS offset of the slice of block 0 (>= 0), or -1 - c
-    // for a chunk read through L2, or kGrpSkip for a padded slot
-    for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
-      const int c = a.order[int64_t(j0) * a.delta + e];
-      int v = kGrpSkip;
-      if (c >= 0 && c < a.N) v = map[c] >= 0 ? map[c] * a.ell * W : -1 - c;
-      code[e] = v;
-    }
-  } else {
-    // one worker (a worker's chunks are distinct): slot t holds position t
-    for (int t = threadIdx.x; t < a.delta; t += kGrpThreads) {
-      const int c = a.order[int64_t(j0) * a.delta + t];
-      const bool ok = c >= 0 && c < a.N;
-      if (t < g.slots) slotc[t] = ok ? c : 0;  // a padded slot stages chunk 0, never read
-      code[t] = !ok ? kGrpSkip : (t < g.slots ? t * a.ell * W : -1 - c);
-    }
-    if (threadIdx.x == 0) nslot = a.delta < g.slots ? a.delta : g.slots;
-    __syncthreads();
-  }
-  // 2. staging of a slice: Gs[(s*ell + k)*W + w] = g_{slotc[s]}[k*L + x0 + w] (zero past L
-  // or d), 16 bytes per thread and step, all of it in registers first; where the compute
-  // leaves room (PREF) the next slice's loads are issued before the current slice is
-  // computed, else each slice is loaded and stored in turn
   const GT *G = reinterpret_cast<const GT *>(a.G);
-  constexpr int SV = 16 / sizeof(GT);
-  const int total = nslot * a.ell * W;
-  uint4 buf[kGrpStage];
-  auto stage_load = [&](int64_t x0) {
-#pragma unroll
-    for (int u = 0; u < kGrpStage; ++u) {
-      int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
-      // recomputed per slice rather than kept live through the compute
-      asm volatile("" : "+v"(e));
-      buf[u] = make_uint4(0u, 0u, 0u, 0u);
-      if (e < total) {
-        const int sk = e / W, w = e % W;
-        const int c = slotc[sk / a.ell], k = sk % a.ell;
-        const int64_t x = x0 + w;
-        const int64_t col = int64_t(k) * a.L + x;
-        const GT *src = G + int64_t(c) * a.d + col;
-        if (a.stage16 && x + SV <= a.L && col + SV <= a.d)
-          buf[u] = *reinterpret_cast<const uint4 *>(src);
-        else
-          buf[u] = load16_guarded(src, x, col, a.L, a.d);
-      }
-    }
-  };
-  auto stage_store = [&]() {
-#pragma unroll
-    for (int u = 0; u < kGrpStage; ++u) {
-      const int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
-      if (e < total) *reinterpret_cast<uint4 *>(Gs + e) = buf[u];
-    }
-  };
-  constexpr bool PREF = PB * NV * VEC <= 16;
-  if constexpr (PREF) stage_load(s_begin * W);
-
-  // 3. items (pattern batch, worker), worker fastest: the waves write neighbouring rows
-  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
-  const int lane = threadIdx.x % kWave;
-  for (int64_t slice = s_begin; slice < s_end; ++slice) {
-  const int64_t x0 = slice * W;
-  __syncthreads();  // tables built; the previous slice's terms all applied
-  if constexpr (!PREF) stage_load(x0);
-  stage_store();
-  __syncthreads();
-  if constexpr (PREF) {
-    if (slice + 1 < s_end) stage_load(x0 + W);
-  }
+  constexpr int W = kWave * VEC * NV;
   const int64_t nb = ceil_div(p1 - p0, PB);
   const int64_t items = nb * nj;
   const int tl = lane % kGrpTerms, pl = lane / kGrpTerms;  // this lane's term and pattern
@@ -402,12 +286,7 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))
     auto term_info = [&](int tk0, float &cv, int &cd) {
       const int tk = tk0 + tl;
       cv = (pl < PB && pb0 + pl < p1 && tk < dl) ? brow[tk] : 0.f;
-      cd = kGrpSkip;
-      if (tk < dl) {
-        const int t = tk / a.ell, k = tk - t * a.ell;
-        const int c0 = code[jb * a.delta + t];
-        cd = c0 == kGrpSkip ? kGrpSkip : (c0 >= 0 ? c0 + k * W : c0 * a.ell - k + (a.ell - 1));
-      }
+      cd = tk < dl ? code[jb * dl + tk] : kGrpSkip;
     };
     float cvn;
     int cdn;
@@ -481,6 +360,252 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))
       }
     }
   }
+}
+
+// The items of one staged slice on the matrix cores, every term of the group staged.
+template <typename GT>
+__device__ __forceinline__ void group_mfma(const EncodeArgs &a, const GT *__restrict__ Gs,
+                                             const int32_t *__restrict__ code, int64_t x0, int j0, int nj,
+                                             int64_t p0, int64_t p1, int wave, int lane) {
+  const int dl = a.delta * a.ell;
+  const GT *G = reinterpret_cast<const GT *>(a.G);
+  constexpr int W = 128;
+  // a wave computes one worker for 32 patterns and 4 x 32 positions on the matrix cores:
+  // D[pattern][x] += A[pattern][term] B[term][x] two terms at a time, A the coefficients
+  // (zero past each pattern's prefix), B the staged slices.  The two terms of step i are
+  // tk0 + i (lanes 0-31) and tk0 + 8 + i (lanes 32-63).
+  const int h = lane >> 5, li = lane & 31;
+  const int64_t items = ceil_div(p1 - p0, 32) * nj;
+  const bool a16 = (dl & 7) == 0 && (reinterpret_cast<uintptr_t>(a.Bc) & 15) == 0;
+  for (int64_t it = wave; it < items; it += kGrpWaves) {
+    const int jb = int(it % nj);
+    const int j = j0 + jb;
+    const int64_t pb0 = p0 + (it / nj) * 32;
+    const int64_t p = pb0 + li;
+    const float *crow = a.Bc + ((p < p1 ? p : pb0) * a.m + j) * int64_t(dl);
+    // this lane's coefficients of terms tk0 + 8h .. + 7 (raw; masked once psi is known),
+    // issued a chunk ahead of their use
+    auto load_a = [&](int tk0, float (&r)[8]) {
+      int tb = tk0 + 8 * h;
+      if (a16) {  // dl a multiple of 8: a lane's eight terms lie all inside the row or all past it
+        if (tb >= dl) tb = 0;  // past the row: values that the prefix mask zeroes
+        const float4 u0 = *reinterpret_cast<const float4 *>(crow + tb);
+        const float4 u1 = *reinterpret_cast<const float4 *>(crow + tb + 4);
+        r[0] = u0.x; r[1] = u0.y; r[2] = u0.z; r[3] = u0.w;
+        r[4] = u1.x; r[5] = u1.y; r[6] = u1.z; r[7] = u1.w;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) r[i] = tb + i < dl ? crow[tb + i] : 0.f;
+      }
+    };
+    float an[8];
+    load_a(0, an);
+    int lim = 0;  // psi*ell of pattern p (0 past the range)
+    if (p < p1) {
+      const int v = a.psi[p * a.m + j];
+      lim = (v < 0 ? 0 : (v > a.delta ? a.delta : v)) * a.ell;
+    }
+    const unsigned long long sendm = __ballot(h == 0 && lim > 0);  // bit i: pattern pb0 + i sends
+    int tmax = lim;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const int v = __shfl_xor(tmax, o, kWave);
+      tmax = v > tmax ? v : tmax;
+    }
+    tmax = __builtin_amdgcn_readfirstlane(tmax);  // equal in every lane
+    if (tmax == 0) continue;  // every pattern of the tile: a straggler, nothing sent
+    v16f acc[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[nt][v] = 0.f;
+    for (int tk0 = 0; tk0 < tmax; tk0 += kGrpTerms) {
+      float av[8];
+      int off[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) av[i] = an[i];
+      load_a(tk0 + kGrpTerms, an);  // unconditional: in-row addresses, masked at use
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int tk = tk0 + 8 * h + i;
+        const int o = tk < dl ? code[jb * dl + tk] : kGrpSkip;
+        off[i] = o >= 0 ? o : 0;  // a padded slot (or past the row): any staged value, times 0
+        av[i] = (tk < lim && o >= 0) ? av[i] : 0.f;  // lim <= dl
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const GT *src = Gs + off[i] + li;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+          acc[nt] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], to_f32<GT>(src[32 * nt]), acc[nt], 0, 0,
+                                                         0);
+      }
+    }
+    // lane (h, li) holds D[8(v/4) + 4h + v%4][li] of each tile
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const int64_t x = x0 + 32 * nt + li;
+      if (x >= a.L) continue;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int pi = 8 * (v >> 2) + 4 * h + (v & 3);
+        if ((sendm >> pi) & 1ull)
+          __builtin_nontemporal_store(acc[nt][v], a.T + ((pb0 + pi) * a.m + j) * a.L + x);
+      }
+    }
+  }
+}
+
+// LDS: [ G slices : slots*ell*W GT ][ code : J*delta*ell int32 ][ slot chunk : slots int32 ][ map : N int32 ]
+// W = 64*VEC*NV: lane l owns x = x0 + (64u + l)*VEC + v for u < NV, v < VEC, so every
+// load and store instruction of a wave covers 64*VEC consecutive positions.
+template <typename GT, int VEC, int NV, int PB, bool MF = false>
+__global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF ? 2 : 4))) void encode_group_kernel(
+    EncodeArgs a, GroupArgs g) {
+  constexpr int W = kWave * VEC * NV;
+  static_assert(MF || (PB >= 1 && PB * kGrpTerms <= kWave), "PB rows of 16 terms fill at most one wave");
+  static_assert(!MF || (W == 4 * 32 && PB == 32), "matrix cores: 32 patterns x 4 tiles of 32 positions");
+  extern __shared__ __align__(16) unsigned char lds[];
+  GT *Gs = reinterpret_cast<GT *>(lds);
+  const size_t gbytes = (size_t(g.slots) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
+  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes);
+  int32_t *slotc = code + g.J * a.delta * a.ell;
+  int32_t *map = slotc + g.slots;  // [N] (dense)
+  __shared__ int nslot, nuni;  // chunks staged; distinct chunks the group uses
+
+  // block -> (slice range, unit = (group, pattern range)).  Blocks are dispatched
+  // round-robin over the 8 XCDs; XCD x takes ranges x, x + 8, ..., and the blocks of all
+  // units of one range run back to back there, so its L2 serves the groups' overlapping
+  // chunk slices.  A block walks its range slice by slice with its group's tables built once.
+  const int64_t b = blockIdx.x;
+  const int64_t units = int64_t(g.ngroups) * g.npr;
+  const int64_t sr = (b & 7) + 8 * ((b >> 3) / units);
+  const int64_t unit = (b >> 3) % units;
+  const int64_t s_begin = sr * g.spb;
+  const int64_t s_end = s_begin + g.spb < a.nslices ? s_begin + g.spb : a.nslices;
+  if (s_begin >= s_end) return;  // the whole block: an empty range at the end
+  const int gi = int(unit % g.ngroups);
+  const int64_t pi = unit / g.ngroups;
+  const int j0 = gi * g.J;
+  const int nj = a.m - j0 < g.J ? a.m - j0 : g.J;
+  const int64_t p0 = pi * g.PR;
+  const int64_t p1 = p0 + g.PR < g.P ? p0 + g.PR : g.P;
+  const int dl = a.delta * a.ell;
+
+  // 1. which chunks the group uses, then slots in ascending chunk order
+  if (g.dense) {
+    for (int c = threadIdx.x; c < a.N; c += kGrpThreads) map[c] = 0;
+    __syncthreads();
+    for (int e = threadIdx.x; e < nj * a.delta; e += kGrpThreads) {
+      const int c = a.order[int64_t(j0) * a.delta + e];  // rows j0.. of order are contiguous
+      if (c >= 0 && c < a.N) map[c] = 1;
+    }
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+      int cnt = 0;
+      for (int base = 0; base < a.N; base += kWave) {
+        const int c = base + int(threadIdx.x);
+        const bool on = c < a.N && map[c] != 0;
+        const unsigned long long mask = __ballot(on);
+        if (on) {
+          const int s_ = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
+          map[c] = s_ < g.slots ? s_ : -1;
+          if (s_ < g.slots) slotc[s_] = c;
+        } else if (c < a.N) {
+          map[c] = -1;
+        }
+        cnt += __popcll(mask);
+      }
+      if (threadIdx.x == 0) {
+        nslot = cnt < g.slots ? cnt : g.slots;
+        nuni = cnt;
+      }
+    }
+    __syncthreads();
+    // per (worker, term tk = t*ell + k): the LDS offset of block k of the chunk at
+    // position t (>= 0), or -1 - (c*ell + k) for a chunk read through L2, or kGrpSkip for
+    // a padded slot
+    const int dlt = a.delta * a.ell;
+    for (int e = threadIdx.x; e < nj * dlt; e += kGrpThreads) {
+      const int jb = e / dlt, tk = e % dlt, t = tk / a.ell, k = tk % a.ell;
+      const int c = a.order[int64_t(j0 + jb) * a.delta + t];
+      int v = kGrpSkip;
+      if (c >= 0 && c < a.N) v = map[c] >= 0 ? (map[c] * a.ell + k) * W : -1 - (c * a.ell + k);
+      code[e] = v;
+    }
+  } else {
+    // one worker (a worker's chunks are distinct): slot t holds position t
+    for (int t = threadIdx.x; t < a.delta; t += kGrpThreads) {
+      const int c = a.order[int64_t(j0) * a.delta + t];
+      const bool ok = c >= 0 && c < a.N;
+      if (t < g.slots) slotc[t] = ok ? c : 0;  // a padded slot stages chunk 0, never read
+      for (int k = 0; k < a.ell; ++k)
+        code[t * a.ell + k] = !ok ? kGrpSkip : (t < g.slots ? (t * a.ell + k) * W : -1 - (c * a.ell + k));
+    }
+    if (threadIdx.x == 0) {
+      nslot = a.delta < g.slots ? a.delta : g.slots;
+      nuni = a.delta;  // every position has a slot when delta <= slots (a padded one: chunk 0)
+    }
+    __syncthreads();
+  }
+  // 2. staging of a slice: Gs[(s*ell + k)*W + w] = g_{slotc[s]}[k*L + x0 + w] (zero past L
+  // or d), 16 bytes per thread and step, all of it in registers first; where the compute
+  // leaves room (PREF) the next slice's loads are issued before the current slice is
+  // computed, else each slice is loaded and stored in turn
+  const GT *G = reinterpret_cast<const GT *>(a.G);
+  constexpr int SV = 16 / sizeof(GT);
+  const int total = nslot * a.ell * W;
+  uint4 buf[kGrpStage];
+  auto stage_load = [&](int64_t x0) {
+#pragma unroll
+    for (int u = 0; u < kGrpStage; ++u) {
+      int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
+      // recomputed per slice rather than kept live through the compute
+      asm volatile("" : "+v"(e));
+      buf[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (e < total) {
+        const int sk = e / W, w = e % W;
+        const int c = slotc[sk / a.ell], k = sk % a.ell;
+        const int64_t x = x0 + w;
+        const int64_t col = int64_t(k) * a.L + x;
+        const GT *src = G + int64_t(c) * a.d + col;
+        if (a.stage16 && x + SV <= a.L && col + SV <= a.d)
+          buf[u] = *reinterpret_cast<const uint4 *>(src);
+        else
+          buf[u] = load16_guarded(src, x, col, a.L, a.d);
+      }
+    }
+  };
+  auto stage_store = [&]() {
+#pragma unroll
+    for (int u = 0; u < kGrpStage; ++u) {
+      const int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
+      if (e < total) *reinterpret_cast<uint4 *>(Gs + e) = buf[u];
+    }
+  };
+  constexpr bool PREF = !MF && PB * NV * VEC <= 16;
+  if constexpr (PREF) stage_load(s_begin * W);
+
+  // 3. items (pattern batch, worker), worker fastest: the waves write neighbouring rows
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+  const int lane = threadIdx.x % kWave;
+  for (int64_t slice = s_begin; slice < s_end; ++slice) {
+  const int64_t x0 = slice * W;
+  __syncthreads();  // tables built; the previous slice's terms all applied
+  if constexpr (!PREF) stage_load(x0);
+  stage_store();
+  __syncthreads();
+  if constexpr (PREF) {
+    if (slice + 1 < s_end) stage_load(x0 + W);
+  }
+  if constexpr (MF) {
+    if (nslot > 0 && nuni <= nslot)
+      group_mfma<GT>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
+    else  // a union past the slots (orders other than the cyclic one): the vector layout
+      group_vector<GT, 2, 1, 4>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
+  } else {
+    group_vector<GT, VEC, NV, PB>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
+  }
   }  // slice
 }
 
@@ -488,7 +613,8 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(4))
 // union of J + delta - 1 chunks), the slice capacity, the patterns per block (staged bytes
 // at most an eighth of those written, where the patterns allow).  Returns the ratio of
 // staged to written bytes, or a negative value when the layout does not fit.
-double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, GroupArgs &g, size_t &lds) {
+double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, int pb, GroupArgs &g,
+                  size_t &lds) {
   const int64_t sb = int64_t(a.ell) * W * int64_t(esize);  // one chunk's slices
   const int64_t B = int64_t(kGrpLds) - 16;
   const int64_t dm1 = a.delta - 1;
@@ -496,16 +622,16 @@ double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, Group
   // groups, whose slots need no map
   g.dense = 4 * int64_t(a.N) <= B / 4 ? 1 : 0;
   const int64_t mapw = g.dense ? a.N : 0;
-  int64_t J = g.dense ? (B - 4 * mapw - (sb + 4) * dm1) / (sb + 4 + 4 * int64_t(a.delta)) : 1;
+  const int64_t dl = int64_t(a.delta) * a.ell;  // table words per worker
+  int64_t J = g.dense ? (B - 4 * mapw - (sb + 4) * dm1) / (sb + 4 + 4 * dl) : 1;
   if (J > a.m) J = a.m;
   if (J < 1) J = 1;
   g.ngroups = int(ceil_div(a.m, J));
   J = ceil_div(a.m, g.ngroups);  // balanced groups
-  int64_t slots = (B - 4 * (J * a.delta + mapw)) / (sb + 4);
+  int64_t slots = (B - 4 * (J * dl + mapw)) / (sb + 4);
   const int64_t most = J * a.delta < a.N ? J * a.delta : a.N;
   if (slots > most) slots = most;
   if (slots < 1) return -1.0;
-  const int pb = P >= 4 ? 4 : 2;
   const int64_t uni = J + dm1 < slots ? J + dm1 : slots;
   int64_t pr = ceil_div(8 * uni * sb, J * W * 4);
   pr = ceil_div(pr < 1 ? 1 : pr, pb) * pb;
@@ -515,20 +641,20 @@ double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, Group
   g.npr = ceil_div(P, pr);
   g.slots = int(slots);
   g.P = P;
-  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + sizeof(int32_t) * size_t(J * a.delta + slots + mapw);
+  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + sizeof(int32_t) * size_t(J * dl + slots + mapw);
   if (lds > kGrpLds) return -1.0;
   return double(uni * sb) / double(J * pr * W * 4);
 }
 
-template <typename GT, int VEC, int NV, int PB>
+template <typename GT, int VEC, int NV, int PB, bool MF = false>
 int launch_group(const EncodeArgs &a, const GroupArgs &g, size_t lds, hipStream_t st) {
   const int64_t blocks = g.nsr * g.ngroups * g.npr;
   if (!grid_ok(blocks, kGrpThreads)) return GC_EINVAL;
-  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_group_kernel<GT, VEC, NV, PB>),
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_group_kernel<GT, VEC, NV, PB, MF>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
     return GC_ELAUNCH;
-  hipLaunchKernelGGL((encode_group_kernel<GT, VEC, NV, PB>), dim3(unsigned(blocks)), dim3(kGrpThreads),
-                     lds, st, a, g);
+  hipLaunchKernelGGL((encode_group_kernel<GT, VEC, NV, PB, MF>), dim3(unsigned(blocks)),
+                     dim3(kGrpThreads), lds, st, a, g);
   return GC_OK;
 }
 
@@ -547,7 +673,8 @@ int pick_group(const EncodeArgs &a, int64_t P, int vec, size_t esize, GroupArgs 
     if (kGrpVec[i] > vec) continue;
     GroupArgs gi{};
     size_t li = 0;
-    if (plan_group(a, P, int64_t(kWave) * kGrpVec[i] * kGrpNv[i], esize, gi, li) < 0) continue;
+    if (plan_group(a, P, int64_t(kWave) * kGrpVec[i] * kGrpNv[i], esize, P >= 4 ? 4 : 2, gi, li) < 0)
+      continue;
     g = gi;
     lds = li;
     pick = i;
@@ -561,11 +688,26 @@ template <typename GT, int VEC>
 int launch_encode_group(EncodeArgs a, int64_t P, hipStream_t st) {
   GroupArgs g{};
   size_t lds = 0;
-  const int c = pick_group(a, P, VEC, sizeof(GT), g, lds);
-  if (c < 0) return GC_EINVAL;
-  a.nslices = int(ceil_div(a.L, int64_t(kWave) * kGrpVec[c] * kGrpNv[c]));
+  // the matrix cores when a call has a full 32-pattern tile and at least 32 terms per
+  // output, and the cyclic union of a group's chunks fits 128 positions wide
+  bool mf = false;
+  if (P >= 32 && a.delta * a.ell >= 32) {
+    GroupArgs gm{};
+    size_t lm = 0;
+    if (plan_group(a, P, 128, sizeof(GT), 32, gm, lm) >= 0) {
+      const int64_t uni = int64_t(gm.J) + a.delta - 1 < a.N ? int64_t(gm.J) + a.delta - 1 : a.N;
+      if (gm.slots >= uni) {
+        g = gm;
+        lds = lm;
+        mf = true;
+      }
+    }
+  }
+  const int c = mf ? -1 : pick_group(a, P, VEC, sizeof(GT), g, lds);
+  if (!mf && c < 0) return GC_EINVAL;
+  a.nslices = int(ceil_div(a.L, mf ? int64_t(128) : int64_t(kWave) * kGrpVec[c] * kGrpNv[c]));
   // enough work units to fill the chip: fewer patterns per block while they are short
-  const int pb = P >= 4 ? 4 : 2;
+  const int pb = mf ? 32 : (P >= 4 ? 4 : 2);
   const int64_t want = 128 * int64_t(cu_count());  // blocks: about 64 rounds of resident ones
   while (a.nslices * g.ngroups * g.npr < want / 2 && g.PR > pb) {
     g.PR = ceil_div(g.PR / 2, pb) * pb;
@@ -577,6 +719,7 @@ int launch_encode_group(EncodeArgs a, int64_t P, hipStream_t st) {
   if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
   g.spb = ceil_div(a.nslices, nsr);
   g.nsr = ceil_div(ceil_div(a.nslices, g.spb), 8) * 8;
+  if (mf) return launch_group<GT, 2, 1, 32, true>(a, g, lds, st);
   const bool pb4 = P >= 4;
   if constexpr (VEC == 4) {
     if (c == 0)

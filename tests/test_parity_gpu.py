@@ -262,6 +262,31 @@ def test_encode_worker_groups(wl, ell, count):
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
 
 
+# matrix-core encode: at least one full 32-pattern tile and delta*ell >= 32 terms per output
+MF_CASES = [
+    (Workload(name="mf_m100_d4096", N=100, m=100, s=9, d=4096, P=40, ells=(8,), pattern="uniform"), 8, 40),
+    (Workload(name="mf_m200_d2001_bf16", N=200, m=200, s=7, d=2001, P=33, ells=(4,), g_dtype="bf16",
+              pattern="uniform"), 4, 33),
+]
+
+
+@pytest.mark.parametrize("wl,ell,count", MF_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in MF_CASES])
+def test_encode_matrix_cores(wl, ell, count):
+    """32-pattern tiles on the matrix cores: a partial last tile, odd L (bf16), padding."""
+    O, order, _, _ = tables(wl)
+    psi = patterns(wl, count)
+    R = gen.shared_R(wl.m, ell)
+    Bc32 = R_.coefficients(O, psi, R)[0].astype(np.float32)
+    G = given_G(wl)
+    Td = torch.full((len(psi), wl.m, -(-wl.d // ell)), float("nan"), device="cuda")
+    T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32), T=Td))
+    T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, wl.g_dtype), ell)
+    sent = psi > 0
+    assert np.isnan(T[~sent]).all()
+    bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
+
+
 @pytest.mark.parametrize("wl,ell", [(TINY, 2), (GROUP_CASES[3][0], 2)], ids=["all-chunk", "worker-group"])
 def test_encode_clamps_psi(wl, ell):
     """psi outside [0, delta] is clamped, in both encode layouts: a negative count sends
