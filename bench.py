@@ -396,7 +396,8 @@ def experiment_shapes(args):
     their parity tests run them: m = 100, d = 2^20 fp32 (48 patterns, ell = 1, 2, 8) and
     m = 200, d = 2^24 bf16 (2 patterns of the 50%-straggler run, ell = 1, 2, 4).  One JSON
     object per (workload, ell): time per call (HIP events, 1 warm-up + 5 calls), bytes of T
-    written / read (transmitting rows only), of G read once, and the rates."""
+    written / read (transmitting rows only), of G read once, the rates, and the estimates
+    decoded per second by encode + combine (coefficients timed separately: decode_large)."""
     import torch
 
     from paper_2405_19509_amd import gcx
@@ -446,6 +447,7 @@ def experiment_shapes(args):
                 "terms_per_output": wl.delta * ell,
                 "encode": {"ms": te, "T_GBps": t_bytes / te / 1e6, "T_plus_G_GBps": (t_bytes + g_bytes) / te / 1e6},
                 "combine": {"ms": tr, "GBps": (t_bytes + 4 * batch * wl.d) / tr / 1e6},
+                "decoded_gradients_per_s": batch / ((te + tr) * 1e-3),
                 "T_bytes": t_bytes, "G_bytes": g_bytes}), flush=True)
             del T, ghat, ws
             torch.cuda.empty_cache()
