@@ -456,22 +456,69 @@ __device__ __forceinline__ void group_mfma(const EncodeArgs &a, const GT *__rest
   }
 }
 
+// The items of one staged slice on the matrix cores with (pattern, worker) rows: the 16 rows
+// of the block (P_block patterns x J workers) against the K staged chunk-block slices,
+// D[row][x] += A[row][k] B[k][x] four terms at a time (v_mfma_f32_16x16x4f32), A the
+// coefficient tile built once per block (zero where a worker does not hold or has not
+// processed a chunk), B the staged slices; each wave owns 32 positions (two 16-wide tiles).
+template <typename GT>
+__device__ __forceinline__ void group_mrows(const EncodeArgs &a, const GT *__restrict__ Gs,
+                                            const float *__restrict__ Asm, int as, int Kp, uint32_t rsend,
+                                            int64_t x0, int j0, int J, int64_t p0, int wave, int lane) {
+  constexpr int W = kGrpWaves * 32;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int xw = wave * 32;
+  v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  const float *arow = Asm + r16 * as + kq;
+  const GT *brow = Gs + kq * W + xw + r16;
+  for (int ks = 0; ks < Kp; ks += 4) {
+    const float av = arow[ks];
+    const GT *bp = brow + ks * W;
+    acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, to_f32<GT>(bp[0]), acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, to_f32<GT>(bp[16]), acc1, 0, 0, 0);
+  }
+  // lane (kq, r16) holds D[4 kq + v][r16] of each tile; rows that do not transmit are skipped
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+    const int64_t x = x0 + xw + 16 * nt + r16;
+    if (x >= a.L) continue;
+    const v4f &acc = nt == 0 ? acc0 : acc1;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = 4 * kq + v;
+      if ((rsend >> i) & 1u) {
+        const int64_t row = (p0 + i / J) * a.m + j0 + i % J;
+        __builtin_nontemporal_store(acc[v], a.T + row * a.L + x);
+      }
+    }
+  }
+}
+
+// rows of staged slices in the matrix-rows layout: a multiple of 4 (zero rows pad K)
+__host__ __device__ inline int mr_rows(int slots, int ell) { return (slots * ell + 3) & ~3; }
+
 // LDS: [ G slices : slots*ell*W GT ][ code : J*delta*ell int32 ][ slot chunk : slots int32 ][ map : N int32 ]
 // W = 64*VEC*NV: lane l owns x = x0 + (64u + l)*VEC + v for u < NV, v < VEC, so every
 // load and store instruction of a wave covers 64*VEC consecutive positions.
-template <typename GT, int VEC, int NV, int PB, bool MF = false>
+template <typename GT, int VEC, int NV, int PB, bool MF = false, bool MR = false>
 __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF ? 2 : 4))) void encode_group_kernel(
     EncodeArgs a, GroupArgs g) {
   constexpr int W = kWave * VEC * NV;
   static_assert(MF || (PB >= 1 && PB * kGrpTerms <= kWave), "PB rows of 16 terms fill at most one wave");
   static_assert(!MF || (W == 4 * 32 && PB == 32), "matrix cores: 32 patterns x 4 tiles of 32 positions");
+  static_assert(!MR || W == kGrpWaves * 32, "matrix rows: each wave two tiles of 16 positions");
   extern __shared__ __align__(16) unsigned char lds[];
   GT *Gs = reinterpret_cast<GT *>(lds);
-  const size_t gbytes = (size_t(g.slots) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
-  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes);
+  const int grows = MR ? mr_rows(g.slots, a.ell) : g.slots * a.ell;  // staged slice rows
+  const size_t gbytes = (size_t(grows) * W * sizeof(GT) + 15) & ~size_t(15);
+  float *Asm = reinterpret_cast<float *>(lds + gbytes);  // MR: [16][grows + 1]
+  const int as = grows + 1;
+  const size_t abytes = MR ? sizeof(float) * 16 * size_t(as) : 0;
+  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes + abytes);
   int32_t *slotc = code + g.J * a.delta * a.ell;
   int32_t *map = slotc + g.slots;  // [N] (dense)
   __shared__ int nslot, nuni;  // chunks staged; distinct chunks the group uses
+  __shared__ uint32_t rsend;   // MR: bit r set when row r (pattern, worker) transmits
 
   // block -> (slice range, unit = (group, pattern range)).  Blocks are dispatched
   // round-robin over the 8 XCDs; XCD x takes ranges x, x + 8, ..., and the blocks of all
@@ -492,6 +539,8 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
   const int64_t p1 = p0 + g.PR < g.P ? p0 + g.PR : g.P;
   const int dl = a.delta * a.ell;
 
+  if constexpr (MR)
+    for (int e = threadIdx.x; e < 16 * as; e += kGrpThreads) Asm[e] = 0.f;
   // 1. which chunks the group uses, then slots in ascending chunk order
   if (g.dense) {
     for (int c = threadIdx.x; c < a.N; c += kGrpThreads) map[c] = 0;
@@ -548,6 +597,37 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
     }
     __syncthreads();
   }
+  if constexpr (MR) {
+    // the coefficient tile: row r = (pattern p0 + r / J, worker j0 + r % J), column
+    // s*ell + k = block k of the chunk in slot s; zero where the worker does not hold the
+    // chunk or has not processed it; and zero rows of slices past the staged ones
+    __syncthreads();
+    const int J = g.J;
+    for (int e = threadIdx.x; e < 16 * a.delta; e += kGrpThreads) {
+      const int r = e / a.delta, t = e % a.delta;
+      const int pb = r / J, jb = r % J;
+      if (p0 + pb >= p1 || jb >= nj) continue;
+      const int64_t p = p0 + pb;
+      const int j = j0 + jb;
+      int v = a.psi[p * a.m + j];
+      v = v < 0 ? 0 : (v > a.delta ? a.delta : v);
+      const int c = a.order[int64_t(j) * a.delta + t];
+      if (t >= v || c < 0 || c >= a.N) continue;
+      const int u = g.dense ? map[c] : (t < g.slots ? t : -1);
+      if (u < 0) continue;
+      const float *src = a.Bc + ((p * a.m + j) * a.delta + t) * a.ell;
+      for (int k = 0; k < a.ell; ++k) Asm[r * as + u * a.ell + k] = src[k];
+    }
+    const int K = nslot * a.ell, Kp = (K + 3) & ~3;
+    for (int e = threadIdx.x; e < (Kp - K) * W; e += kGrpThreads) Gs[K * W + e] = GT(0);
+    if (threadIdx.x < kWave) {
+      bool on = false;
+      const int r = int(threadIdx.x), pb = r / J, jb = r % J;
+      if (r < 16 && p0 + pb < p1 && jb < nj) on = a.psi[(p0 + pb) * a.m + j0 + jb] > 0;
+      const unsigned long long mask = __ballot(on);
+      if (threadIdx.x == 0) rsend = uint32_t(mask);
+    }
+  }
   // 2. staging of a slice: Gs[(s*ell + k)*W + w] = g_{slotc[s]}[k*L + x0 + w] (zero past L
   // or d), 16 bytes per thread and step, all of it in registers first; where the compute
   // leaves room (PREF) the next slice's loads are issued before the current slice is
@@ -603,6 +683,11 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
       group_mfma<GT>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
     else  // a union past the slots (orders other than the cyclic one): the vector layout
       group_vector<GT, 2, 1, 4>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
+  } else if constexpr (MR) {
+    if (nslot > 0 && nuni <= nslot)
+      group_mrows<GT>(a, Gs, Asm, as, (nslot * a.ell + 3) & ~3, rsend, x0, j0, g.J, p0, wave, lane);
+    else
+      group_vector<GT, VEC, NV, PB>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
   } else {
     group_vector<GT, VEC, NV, PB>(a, Gs, code, x0, j0, nj, p0, p1, wave, lane);
   }
@@ -646,14 +731,48 @@ double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, int p
   return double(uni * sb) / double(J * pr * W * 4);
 }
 
-template <typename GT, int VEC, int NV, int PB, bool MF = false>
+// Sizes of the matrix-rows layout (fewer than 32 patterns per call, many terms): 16 rows of
+// (pattern, worker) per block, P_block = min(P, 16) patterns by J = 16 / P_block workers; the
+// cyclic union of the group's chunks must fit, with the coefficient tile, in the LDS budget.
+bool plan_rows(const EncodeArgs &a, int64_t P, size_t esize, GroupArgs &g, size_t &lds) {
+  const int64_t W = kGrpWaves * 32;
+  const int64_t sb = int64_t(a.ell) * W * int64_t(esize);
+  const int64_t B = int64_t(kGrpLds) - 16;
+  const int pblk = P < 16 ? int(P) : 16;
+  int64_t J = 16 / pblk;
+  if (J > a.m) J = a.m;
+  g.dense = 4 * int64_t(a.N) <= B / 4 ? 1 : 0;
+  if (!g.dense) J = 1;
+  g.ngroups = int(ceil_div(a.m, J));
+  J = ceil_div(a.m, g.ngroups);  // balanced groups
+  const int64_t dl = int64_t(a.delta) * a.ell, mapw = g.dense ? a.N : 0;
+  // per slot: its slices, its coefficient columns, its slot word; fixed: the per-term table,
+  // the map, the tile's padding column and up to three zero rows of slices
+  const int64_t fixed = 4 * (J * dl + mapw) + 16 * 4 * 4 + 3 * W * int64_t(esize);
+  int64_t slots = (B - fixed) / (sb + 64 * a.ell + 4);
+  const int64_t most = J * a.delta < a.N ? J * a.delta : a.N;
+  if (slots > most) slots = most;
+  const int64_t need = J + a.delta - 1 < a.N ? J + a.delta - 1 : a.N;
+  if (slots < need || slots < 1) return false;
+  g.J = int(J);
+  g.PR = pblk;
+  g.npr = ceil_div(P, pblk);
+  g.slots = int(slots);
+  g.P = P;
+  const int gr = mr_rows(int(slots), a.ell);
+  lds = ((size_t(gr) * W * esize + 15) & ~size_t(15)) + sizeof(float) * 16 * size_t(gr + 1) +
+        sizeof(int32_t) * size_t(J * dl + slots + mapw);
+  return lds <= kGrpLds;
+}
+
+template <typename GT, int VEC, int NV, int PB, bool MF = false, bool MR = false>
 int launch_group(const EncodeArgs &a, const GroupArgs &g, size_t lds, hipStream_t st) {
   const int64_t blocks = g.nsr * g.ngroups * g.npr;
   if (!grid_ok(blocks, kGrpThreads)) return GC_EINVAL;
-  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_group_kernel<GT, VEC, NV, PB, MF>),
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_group_kernel<GT, VEC, NV, PB, MF, MR>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
     return GC_ELAUNCH;
-  hipLaunchKernelGGL((encode_group_kernel<GT, VEC, NV, PB, MF>), dim3(unsigned(blocks)),
+  hipLaunchKernelGGL((encode_group_kernel<GT, VEC, NV, PB, MF, MR>), dim3(unsigned(blocks)),
                      dim3(kGrpThreads), lds, st, a, g);
   return GC_OK;
 }
@@ -703,11 +822,23 @@ int launch_encode_group(EncodeArgs a, int64_t P, hipStream_t st) {
       }
     }
   }
-  const int c = mf ? -1 : pick_group(a, P, VEC, sizeof(GT), g, lds);
-  if (!mf && c < 0) return GC_EINVAL;
-  a.nslices = int(ceil_div(a.L, mf ? int64_t(128) : int64_t(kWave) * kGrpVec[c] * kGrpNv[c]));
+  // fewer patterns per call: the matrix cores with (pattern, worker) rows, 256 positions wide
+  bool mr = false;
+  if (!mf && P < 32 && a.delta * a.ell >= 32) {
+    GroupArgs gr{};
+    size_t lr = 0;
+    if (plan_rows(a, P, sizeof(GT), gr, lr)) {
+      g = gr;
+      lds = lr;
+      mr = true;
+    }
+  }
+  const int c = (mf || mr) ? -1 : pick_group(a, P, VEC, sizeof(GT), g, lds);
+  if (!mf && !mr && c < 0) return GC_EINVAL;
+  const int64_t W = mf ? 128 : (mr ? int64_t(kGrpWaves) * 32 : int64_t(kWave) * kGrpVec[c] * kGrpNv[c]);
+  a.nslices = int(ceil_div(a.L, W));
   // enough work units to fill the chip: fewer patterns per block while they are short
-  const int pb = mf ? 32 : (P >= 4 ? 4 : 2);
+  const int pb = mf ? 32 : (mr ? int(g.PR) : (P >= 4 ? 4 : 2));
   const int64_t want = 128 * int64_t(cu_count());  // blocks: about 64 rounds of resident ones
   while (a.nslices * g.ngroups * g.npr < want / 2 && g.PR > pb) {
     g.PR = ceil_div(g.PR / 2, pb) * pb;
@@ -720,6 +851,9 @@ int launch_encode_group(EncodeArgs a, int64_t P, hipStream_t st) {
   g.spb = ceil_div(a.nslices, nsr);
   g.nsr = ceil_div(ceil_div(a.nslices, g.spb), 8) * 8;
   if (mf) return launch_group<GT, 2, 1, 32, true>(a, g, lds, st);
+  if (mr)
+    return P >= 4 ? launch_group<GT, 1, 4, 4, false, true>(a, g, lds, st)
+                  : launch_group<GT, 1, 4, 2, false, true>(a, g, lds, st);
   const bool pb4 = P >= 4;
   if constexpr (VEC == 4) {
     if (c == 0)

@@ -287,6 +287,48 @@ def test_encode_matrix_cores(wl, ell, count):
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
 
 
+# matrix-core encode with (pattern, worker) rows: fewer than 32 patterns per call, >= 32 terms
+MR_WL = Workload(name="mr_m100_d4099", N=100, m=100, s=15, d=4099, P=16, ells=(2,), pattern="uniform")
+MR_WL_BF16 = Workload(name="mr_m200_d4001_bf16", N=200, m=200, s=19, d=4001, P=3, ells=(4,),
+                      g_dtype="bf16", pattern="uniform")
+MR_CASES = [(MR_WL, 2, 1), (MR_WL, 2, 2), (MR_WL, 2, 7), (MR_WL, 2, 16), (MR_WL_BF16, 4, 3)]
+
+
+def _encode_against_oracle(O, order, psi, R, G, g_dtype, ell, d):
+    Bc32 = R_.coefficients(O, psi, R)[0].astype(np.float32)
+    Gt = dev(G.view(np.int16)).view(torch.bfloat16) if g_dtype == "bf16" else dev(G)
+    Td = torch.full((len(psi), O.shape[1], -(-d // ell)), float("nan"), device="cuda")
+    T = host(gcx.gc_encode(Gt, dev(psi), dev(order), dev(Bc32), T=Td))
+    T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, g_dtype), ell)
+    sent = psi > 0
+    assert np.isnan(T[~sent]).all()
+    bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
+
+
+@pytest.mark.parametrize("wl,ell,count", MR_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in MR_CASES])
+def test_encode_matrix_rows(wl, ell, count):
+    """16 rows of (pattern, worker) per tile on the matrix cores: 1 to 16 patterns per call,
+    odd L, padding, bf16."""
+    O, order, _, _ = tables(wl)
+    _encode_against_oracle(O, order, patterns(wl, count), gen.shared_R(wl.m, ell), given_G(wl),
+                           wl.g_dtype, ell, wl.d)
+
+
+def test_encode_matrix_rows_spilled_union():
+    """A random 16-regular support (Algorithm 2 ordering): the chunks of 8 workers no longer fit
+    the matrix-rows layout's slots, so its blocks take the vector path."""
+    import oracle.ordering as OO
+    m, nu, ell, d = 100, 16, 2, 4099
+    A = gen.random_regular_graph(m, nu)
+    O = OO.chunk_ordering(A)
+    _, order, _, _ = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, m, m, -1, O.astype(np.int32), nu, nu)
+    g = np.random.default_rng(41)
+    psi = g.integers(0, nu + 1, size=(2, m)).astype(np.int32)
+    G = g.standard_normal((m, d)).astype(np.float32)
+    _encode_against_oracle(O.astype(np.int64), order, psi, gen.shared_R(m, ell), G, "f32", ell, d)
+
+
 @pytest.mark.parametrize("wl,ell", [(TINY, 2), (GROUP_CASES[3][0], 2)], ids=["all-chunk", "worker-group"])
 def test_encode_clamps_psi(wl, ell):
     """psi outside [0, delta] is clamped, in both encode layouts: a negative count sends
