@@ -213,7 +213,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
 // contraction [32 patterns][terms] x [terms][128 positions] per worker), a block whose
 // group's chunks are all staged runs its items on the matrix cores instead
 // (v_mfma_f32_32x32x2f32; coefficients past a pattern's prefix enter as zeros, so the
-// gradient values must be finite).
+// gradient values must be finite).  With fewer patterns, the tile rows are 16 (pattern,
+// worker) pairs and its K the group's staged chunk blocks (v_mfma_f32_16x16x4f32).
 constexpr int kGrpThreads = 512;
 constexpr int kGrpWaves = kGrpThreads / kWave;
 constexpr size_t kGrpLds = 72 * 1024;  // per block: two blocks per CU
