@@ -217,30 +217,26 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
 // worker) pairs and its K the group's staged chunk blocks (v_mfma_f32_16x16x4f32).
 constexpr int kGrpThreads = 512;
 constexpr int kGrpWaves = kGrpThreads / kWave;
-constexpr size_t kGrpLds = 72 * 1024;  // per block: two blocks per CU
+constexpr size_t kGrpLds = 72 * 1024;     // per block: two blocks per CU
+constexpr size_t kGrpLdsMF = 144 * 1024;  // matrix cores, 32-pattern tiles: one block per CU
 static_assert(kGrpLds <= size_t(9) * 512 * 16, "one staging pass covers the slice budget");
 constexpr int kGrpTerms = 16;          // terms per coefficient load
 constexpr int kGrpStage = 9;           // 16-byte staging loads per thread: the whole slice
 constexpr int kGrpSkip = INT32_MIN;    // a padded order slot: no term
 
-// 16 bytes of G from src (positions x.. of block column col..), zero past L or past d
-__device__ __forceinline__ uint32_t pick16(const float *src, int v, bool ok) {
-  return ok ? __float_as_uint(src[v]) : 0u;
-}
-__device__ __forceinline__ uint4 load16_guarded(const float *src, int64_t x, int64_t col, int64_t L,
-                                                int64_t d) {
+// 16 bytes of G from src (positions x.. of a block row valid below lim), zero from lim on
+__device__ __forceinline__ uint4 load16_lim(const float *src, int64_t x, int64_t lim) {
   uint32_t r[4];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) r[v] = pick16(src, v, x + v < L && col + v < d);
+  for (int v = 0; v < 4; ++v) r[v] = x + v < lim ? __float_as_uint(src[v]) : 0u;
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
-__device__ __forceinline__ uint4 load16_guarded(const uint16_t *src, int64_t x, int64_t col, int64_t L,
-                                                int64_t d) {
+__device__ __forceinline__ uint4 load16_lim(const uint16_t *src, int64_t x, int64_t lim) {
   uint32_t r[4];
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
-    const uint32_t lo = (x + 2 * v < L && col + 2 * v < d) ? src[2 * v] : 0u;
-    const uint32_t hi = (x + 2 * v + 1 < L && col + 2 * v + 1 < d) ? src[2 * v + 1] : 0u;
+    const uint32_t lo = x + 2 * v < lim ? src[2 * v] : 0u;
+    const uint32_t hi = x + 2 * v + 1 < lim ? src[2 * v + 1] : 0u;
     r[v] = lo | (hi << 16);
   }
   return make_uint4(r[0], r[1], r[2], r[3]);
@@ -515,7 +511,10 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
   float *Asm = reinterpret_cast<float *>(lds + gbytes);  // MR: [16][grows + 1]
   const int as = grows + 1;
   const size_t abytes = MR ? sizeof(float) * 16 * size_t(as) : 0;
-  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes + abytes);
+  // per staged row s*ell + k: element offset of block k of chunk slotc[s] in G, and the end
+  // of that block's valid positions (min(L, d - k*L))
+  int64_t *rdesc = reinterpret_cast<int64_t *>(lds + gbytes + abytes);
+  int32_t *code = reinterpret_cast<int32_t *>(lds + gbytes + abytes + 2 * sizeof(int64_t) * size_t(grows));
   int32_t *slotc = code + g.J * a.delta * a.ell;
   int32_t *map = slotc + g.slots;  // [N] (dense)
   __shared__ int nslot, nuni;  // chunks staged; distinct chunks the group uses
@@ -629,6 +628,13 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
       if (threadIdx.x == 0) rsend = uint32_t(mask);
     }
   }
+  for (int row = threadIdx.x; row < nslot * a.ell; row += kGrpThreads) {
+    const int sl = row / a.ell, k = row % a.ell;
+    rdesc[2 * row] = int64_t(slotc[sl]) * a.d + int64_t(k) * a.L;
+    const int64_t rem = a.d - int64_t(k) * a.L;
+    rdesc[2 * row + 1] = rem < a.L ? rem : a.L;
+  }
+  __syncthreads();
   // 2. staging of a slice: Gs[(s*ell + k)*W + w] = g_{slotc[s]}[k*L + x0 + w] (zero past L
   // or d), 16 bytes per thread and step, all of it in registers first; where the compute
   // leaves room (PREF) the next slice's loads are issued before the current slice is
@@ -637,30 +643,29 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
   constexpr int SV = 16 / sizeof(GT);
   const int total = nslot * a.ell * W;
   uint4 buf[kGrpStage];
-  auto stage_load = [&](int64_t x0) {
+  // one pass covers kGrpStage * kGrpThreads * 16 bytes from element e0 on
+  auto stage_load = [&](int64_t x0, int e0 = 0) {
 #pragma unroll
     for (int u = 0; u < kGrpStage; ++u) {
-      int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
+      int e = e0 + (int(threadIdx.x) + u * kGrpThreads) * SV;
       // recomputed per slice rather than kept live through the compute
       asm volatile("" : "+v"(e));
       buf[u] = make_uint4(0u, 0u, 0u, 0u);
       if (e < total) {
-        const int sk = e / W, w = e % W;
-        const int c = slotc[sk / a.ell], k = sk % a.ell;
-        const int64_t x = x0 + w;
-        const int64_t col = int64_t(k) * a.L + x;
-        const GT *src = G + int64_t(c) * a.d + col;
-        if (a.stage16 && x + SV <= a.L && col + SV <= a.d)
+        const int row = e / W, w = e % W;
+        const int64_t x = x0 + w, lim = rdesc[2 * row + 1];
+        const GT *src = G + rdesc[2 * row] + x;
+        if (a.stage16 && x + SV <= lim)
           buf[u] = *reinterpret_cast<const uint4 *>(src);
         else
-          buf[u] = load16_guarded(src, x, col, a.L, a.d);
+          buf[u] = load16_lim(src, x, lim);
       }
     }
   };
-  auto stage_store = [&]() {
+  auto stage_store = [&](int e0 = 0) {
 #pragma unroll
     for (int u = 0; u < kGrpStage; ++u) {
-      const int e = (int(threadIdx.x) + u * kGrpThreads) * SV;
+      const int e = e0 + (int(threadIdx.x) + u * kGrpThreads) * SV;
       if (e < total) *reinterpret_cast<uint4 *>(Gs + e) = buf[u];
     }
   };
@@ -673,8 +678,14 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
   for (int64_t slice = s_begin; slice < s_end; ++slice) {
   const int64_t x0 = slice * W;
   __syncthreads();  // tables built; the previous slice's terms all applied
-  if constexpr (!PREF) stage_load(x0);
-  stage_store();
+  if constexpr (!PREF) {
+    for (int e0 = 0; e0 < total; e0 += kGrpStage * kGrpThreads * SV) {
+      stage_load(x0, e0);
+      stage_store(e0);
+    }
+  } else {
+    stage_store();
+  }
   __syncthreads();
   if constexpr (PREF) {
     if (slice + 1 < s_end) stage_load(x0 + W);
@@ -700,21 +711,21 @@ __global__ __launch_bounds__(kGrpThreads) __attribute__((amdgpu_waves_per_eu(MF 
 // at most an eighth of those written, where the patterns allow).  Returns the ratio of
 // staged to written bytes, or a negative value when the layout does not fit.
 double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, int pb, GroupArgs &g,
-                  size_t &lds) {
+                  size_t &lds, size_t budget = kGrpLds) {
   const int64_t sb = int64_t(a.ell) * W * int64_t(esize);  // one chunk's slices
-  const int64_t B = int64_t(kGrpLds) - 16;
+  const int64_t B = int64_t(budget) - 16;
   const int64_t dm1 = a.delta - 1;
   // the dense chunk map needs 4N bytes; past a quarter of the budget, single-worker
   // groups, whose slots need no map
-  g.dense = 4 * int64_t(a.N) <= B / 4 ? 1 : 0;
+  g.dense = 4 * int64_t(a.N) <= (int64_t(kGrpLds) - 16) / 4 ? 1 : 0;
   const int64_t mapw = g.dense ? a.N : 0;
   const int64_t dl = int64_t(a.delta) * a.ell;  // table words per worker
-  int64_t J = g.dense ? (B - 4 * mapw - (sb + 4) * dm1) / (sb + 4 + 4 * dl) : 1;
+  int64_t J = g.dense ? (B - 4 * mapw - (sb + 4 + 16 * a.ell) * dm1) / (sb + 4 + 16 * a.ell + 4 * dl) : 1;
   if (J > a.m) J = a.m;
   if (J < 1) J = 1;
   g.ngroups = int(ceil_div(a.m, J));
   J = ceil_div(a.m, g.ngroups);  // balanced groups
-  int64_t slots = (B - 4 * (J * dl + mapw)) / (sb + 4);
+  int64_t slots = (B - 4 * (J * dl + mapw)) / (sb + 4 + 16 * a.ell);
   const int64_t most = J * a.delta < a.N ? J * a.delta : a.N;
   if (slots > most) slots = most;
   if (slots < 1) return -1.0;
@@ -727,8 +738,9 @@ double plan_group(const EncodeArgs &a, int64_t P, int64_t W, size_t esize, int p
   g.npr = ceil_div(P, pr);
   g.slots = int(slots);
   g.P = P;
-  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + sizeof(int32_t) * size_t(J * dl + slots + mapw);
-  if (lds > kGrpLds) return -1.0;
+  lds = ((size_t(sb) * slots + 15) & ~size_t(15)) + 2 * sizeof(int64_t) * size_t(slots) * a.ell +
+        sizeof(int32_t) * size_t(J * dl + slots + mapw);
+  if (lds > budget) return -1.0;
   return double(uni * sb) / double(J * pr * W * 4);
 }
 
@@ -749,8 +761,8 @@ bool plan_rows(const EncodeArgs &a, int64_t P, size_t esize, GroupArgs &g, size_
   const int64_t dl = int64_t(a.delta) * a.ell, mapw = g.dense ? a.N : 0;
   // per slot: its slices, its coefficient columns, its slot word; fixed: the per-term table,
   // the map, the tile's padding column and up to three zero rows of slices
-  const int64_t fixed = 4 * (J * dl + mapw) + 16 * 4 * 4 + 3 * W * int64_t(esize);
-  int64_t slots = (B - fixed) / (sb + 64 * a.ell + 4);
+  const int64_t fixed = 4 * (J * dl + mapw) + 16 * 4 * 4 + 3 * (W * int64_t(esize) + 16);
+  int64_t slots = (B - fixed) / (sb + 64 * a.ell + 16 * a.ell + 4);
   const int64_t most = J * a.delta < a.N ? J * a.delta : a.N;
   if (slots > most) slots = most;
   const int64_t need = J + a.delta - 1 < a.N ? J + a.delta - 1 : a.N;
@@ -762,7 +774,7 @@ bool plan_rows(const EncodeArgs &a, int64_t P, size_t esize, GroupArgs &g, size_
   g.P = P;
   const int gr = mr_rows(int(slots), a.ell);
   lds = ((size_t(gr) * W * esize + 15) & ~size_t(15)) + sizeof(float) * 16 * size_t(gr + 1) +
-        sizeof(int32_t) * size_t(J * dl + slots + mapw);
+        2 * sizeof(int64_t) * size_t(gr) + sizeof(int32_t) * size_t(J * dl + slots + mapw);
   return lds <= kGrpLds;
 }
 
@@ -814,7 +826,7 @@ int launch_encode_group(EncodeArgs a, int64_t P, hipStream_t st) {
   if (P >= 32 && a.delta * a.ell >= 32) {
     GroupArgs gm{};
     size_t lm = 0;
-    if (plan_group(a, P, 128, sizeof(GT), 32, gm, lm) >= 0) {
+    if (plan_group(a, P, 128, sizeof(GT), 32, gm, lm, kGrpLdsMF) >= 0) {
       const int64_t uni = int64_t(gm.J) + a.delta - 1 < a.N ? int64_t(gm.J) + a.delta - 1 : a.N;
       if (gm.slots >= uni) {
         g = gm;
