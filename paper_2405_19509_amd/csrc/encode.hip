@@ -4,18 +4,24 @@
 // their rows of T are not written.
 //
 // Bandwidth design (HBM-bound on the T write, ~1 flop per byte):
-//   - a block owns one slice of W consecutive x positions and a contiguous
-//     range of rows r = p*m + j;  it stages the W-wide slice of every block k
-//     of every chunk gradient in LDS once (N*ell*W values, stored type), so
-//     the ~psi*ell reads per output element hit LDS, not HBM or L2;
-//   - per-row metadata (psi, the chunk indices and the coefficients of the
-//     row's processed prefix) is staged group by group in LDS with coalesced
-//     loads, then read back as wave-uniform broadcasts;
-//   - a wave writes one row segment of W floats (64 lanes x VEC floats)
-//     per row: fully coalesced, and every T byte is written exactly once;
-//   - block -> (slice, row range) is XCD-aware: blocks are dispatched
-//     round-robin over the 8 XCDs, and every block of a slice runs on the
-//     same XCD, so its L2 serves the repeated slice staging.
+//   - a block owns one slice of W consecutive x positions and a run of about 512
+//     consecutive rows r = p*m + j; it stages the W-wide slice of every block k
+//     of every chunk gradient in LDS (N*ell*W values, stored type), straight
+//     from memory to LDS with every piece in flight at once, so the ~psi*ell
+//     reads per output element hit LDS, not HBM or L2;
+//   - the rows' metadata is staged group by group as a table of (LDS offset,
+//     coefficient) per term, four terms per pair of 16-byte LDS reads; its loads
+//     are independent of each other (one round trip per group);
+//   - a wave writes one row segment of W floats (64 lanes x VEC floats) per
+//     row: fully coalesced, and every T byte is written exactly once;
+//   - the run length trades the slice staging (N*ell*W values per block, from
+//     L2) against the spread of the write front: the blocks in flight cover
+//     every slice of a few thousand rows, and runs of ~512 rows wrote T ~5%
+//     faster than runs of 4096 (runs of 64-128 lose more to the per-block
+//     staging and latency than they gain);
+//   - block -> (slice, row run) is XCD-aware: blocks are dispatched round-robin
+//     over the 8 XCDs, and every block of a slice runs on the same XCD, so its
+//     L2 serves the repeated slice staging.
 // When the slice of every chunk does not fit in LDS (many chunks, ell >= 2, bf16 at
 // large N) the worker-group layout below takes over.
 #include "common.h"
@@ -27,8 +33,8 @@ constexpr int kEncThreads = 1024;
 constexpr int kEncWaves = kEncThreads / kWave;
 constexpr size_t kEncSliceLds = 96 * 1024;   // G slice budget
 constexpr size_t kEncMetaLds = 24 * 1024;    // row metadata budget
-constexpr int64_t kEncRowsPerBlock = 4096;
-constexpr int kEncMaxGroup = 1024;           // rows of metadata staged per step, at most
+constexpr int kEncGroup = 256;               // rows of metadata staged per step, at most
+constexpr int kEncGroupsPerBlock = 2;        // rows per block = 2 groups
 
 template <typename GT>
 __device__ __forceinline__ float to_f32(GT v);
@@ -80,6 +86,13 @@ __device__ __forceinline__ void store_vec(float *p, const float (&v)[VEC]) {
   }
 }
 
+// 16 bytes per lane from global memory straight into LDS: lane i of the wave writes
+// bytes 16i..16i+15 of the 1 KB run at `lds_run` (which must be the same for every lane).
+// Completion is counted by vmcnt like any vector load.
+__device__ __forceinline__ void load_lds16(const void *src, void *lds_run) {
+  __builtin_amdgcn_global_load_lds(src, lds_run, 16, 0, 0);
+}
+
 struct EncodeArgs {
   const void *G;
   int N;
@@ -96,21 +109,32 @@ struct EncodeArgs {
   int nslices;
   int64_t rows_per_block;
   int group_rows;  // rows of metadata staged per step
+  int term_stride; // delta*ell rounded up to 4
   bool stage16;    // d and L multiples of 16 bytes of G, G 16-byte aligned
 };
 
-// LDS layout: [ G slice : N*ell*W GT ][ psi : group ][ chunk : group*delta ][ coef : group*delta*ell ]
+// LDS layout: [ G slice : N*ell*W GT ][ zero row : W GT ][ nterm : group ][ off : group*SR ]
+//             [ coef : group*SR ],  SR = delta*ell rounded up to 4.
+// Row e's terms u < SR: off = LDS element offset of the slice term u reads (chunk
+// order[j][u / ell], block u % ell), coef its coefficient; terms past the row's processed
+// prefix, and chunk indices outside [0, N), read the zero row with coefficient 0.
+// nterm = the row's psi*ell rounded up to 4 (0: the row transmits nothing).
 template <typename GT, int VEC>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   constexpr int W = kWave * VEC;
+  constexpr int SV = 16 / sizeof(GT);  // elements per 16-byte piece
+  constexpr int PPR = W / SV;          // pieces per staged row
   extern __shared__ __align__(16) unsigned char lds[];
   GT *Gs = reinterpret_cast<GT *>(lds);
-  const size_t gbytes = (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
-  int32_t *mpsi = reinterpret_cast<int32_t *>(lds + gbytes);
-  int32_t *mchunk = mpsi + a.group_rows;
-  float *mcoef = reinterpret_cast<float *>(mchunk + size_t(a.group_rows) * a.delta);
+  const int nrow = a.N * a.ell;
+  const size_t gbytes = size_t(nrow + 1) * W * sizeof(GT);  // W*sizeof(GT) is a multiple of 16
+  const int SR = a.term_stride;
+  int32_t *mnt = reinterpret_cast<int32_t *>(lds + gbytes);
+  int32_t *moff = mnt + ((a.group_rows + 3) & ~3);
+  float *mcoef = reinterpret_cast<float *>(moff + size_t(a.group_rows) * SR);
+  const int zoff = nrow * W;
 
-  // block -> (slice, row block); every block of a slice lands on one XCD
+  // block -> (slice, row run); every block of a slice lands on one XCD
   const int64_t b = blockIdx.x;
   int64_t slice, rblock;
   if ((a.nslices & 7) == 0) {
@@ -124,72 +148,77 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
   const int64_t x0 = slice * W;
   const int64_t r0 = rblock * a.rows_per_block;
   const int64_t r1 = r0 + a.rows_per_block < a.rows ? r0 + a.rows_per_block : a.rows;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
 
-  // stage the slice: Gs[(c*ell + k)*W + w] = g_c[k*L + x0 + w] (zero past L or past d),
-  // 16 bytes per load where the run lies inside the gradient (d, L and G aligned to it)
+  // the slice: Gs[(c*ell + k)*W + w] = g_c[k*L + x0 + w] (zero past L or past d).  A
+  // 16-byte piece inside the gradient (d, L and G aligned to it) goes straight from
+  // memory to LDS (global_load_lds_dwordx4: lane i of a wave fills bytes 16i..16i+15
+  // of the wave's 1 KB run), every piece in flight at once; the rest element by element.
   const GT *G = reinterpret_cast<const GT *>(a.G);
-  const int nrow = a.N * a.ell;
-  constexpr int SV = 16 / sizeof(GT);
-  using SVT = uint4;
-  for (int e = threadIdx.x * SV; e < nrow * W; e += kEncThreads * SV) {
-    const int ck = e / W, w = e % W;  // W is a multiple of SV
-    const int c = ck / a.ell, k = ck % a.ell;
+  const int npieces = nrow * PPR;
+  for (int p0 = 0; p0 < npieces; p0 += kEncThreads) {
+    const int p = p0 + int(threadIdx.x);
+    const int ck = p / PPR, w = (p % PPR) * SV;
+    const int c = ck / a.ell, k = ck - c * a.ell;
     const int64_t x = x0 + w;
     const int64_t col = int64_t(k) * a.L + x;
-    if (a.stage16 && x + SV <= a.L && col + SV <= a.d) {
-      *reinterpret_cast<SVT *>(Gs + e) = *reinterpret_cast<const SVT *>(G + int64_t(c) * a.d + col);
-    } else {
-#pragma unroll
+    const bool fast = p < npieces && a.stage16 && x + SV <= a.L && col + SV <= a.d;
+    if (fast) load_lds16(G + int64_t(c) * a.d + col, Gs + size_t(p0 + wave * kWave) * SV);
+    else if (p < npieces)
       for (int u = 0; u < SV; ++u)
-        Gs[e + u] = (x + u < a.L && col + u < a.d) ? G[int64_t(c) * a.d + col + u] : GT(0);
-    }
+        Gs[size_t(p) * SV + u] = (x + u < a.L && col + u < a.d) ? G[int64_t(c) * a.d + col + u] : GT(0);
   }
+  for (int e = threadIdx.x; e < W; e += kEncThreads) Gs[zoff + e] = GT(0);
 
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int stride_row = a.delta * a.ell;
   const int64_t xl = x0 + int64_t(lane) * VEC;  // this lane's first x
-  __shared__ int nact;                          // rows of the group that transmit
-  __shared__ int16_t act[kEncMaxGroup];
   for (int64_t g0 = r0; g0 < r1; g0 += a.group_rows) {
     const int gn = int(r1 - g0 < a.group_rows ? r1 - g0 : a.group_rows);
-    __syncthreads();  // previous group fully consumed (and the slice staged)
-    if (threadIdx.x == 0) nact = 0;
-    __syncthreads();
-    for (int e = threadIdx.x; e < gn; e += kEncThreads) {
-      const int64_t r = g0 + e;
-      const int j = int(r % a.m);
-      int v = a.psi[r];
-      v = v < 0 ? 0 : (v > a.delta ? a.delta : v);
-      mpsi[e] = v;
-      // a worker that has processed nothing transmits nothing: only the other
-      // rows are queued, so the waves share the transmitted rows evenly
-      if (v > 0) act[atomicAdd(&nact, 1)] = int16_t(e);
-      for (int t = 0; t < a.delta; ++t) {
-        int c = a.order[int64_t(j) * a.delta + t];
-        mchunk[e * a.delta + t] = (c >= 0 && c < a.N) ? c : -1;
+    if (g0 != r0) __syncthreads();  // previous group fully consumed
+    for (int e = threadIdx.x; e < gn * SR; e += kEncThreads) {
+      const int row = e / SR, u = e - row * SR;
+      const int64_t r = g0 + row;
+      // three independent loads (one round trip), then the selection
+      int np = a.psi[r];
+      const int t = u / a.ell, k = u - t * a.ell;
+      int c = -1;
+      float w = 0.f;
+      if (u < a.delta * a.ell) {
+        c = a.order[int64_t(r % a.m) * a.delta + t];
+        w = a.Bc[r * a.delta * a.ell + u];
       }
+      np = np < 0 ? 0 : (np > a.delta ? a.delta : np);
+      const bool live = u < np * a.ell && c >= 0 && c < a.N;
+      moff[e] = live ? (c * a.ell + k) * W : zoff;
+      mcoef[e] = live ? w : 0.f;
+      if (u == 0) mnt[row] = (np * a.ell + 3) & ~3;
     }
-    const float *src = a.Bc + g0 * stride_row;
-    for (int e = threadIdx.x; e < gn * stride_row; e += kEncThreads) mcoef[e] = src[e];
+    __builtin_amdgcn_s_waitcnt(0);  // the slice's direct-to-LDS loads have landed
     __syncthreads();
 
-    const int na = nact;
-    for (int ai = wave; ai < na; ai += kEncWaves) {
-      const int e = act[ai];
+    // a worker that has processed nothing transmits nothing: its row is skipped
+    for (int e = wave; e < gn; e += kEncWaves) {
+      const int nt = mnt[e];
+      if (nt == 0) continue;
       const int64_t r = g0 + e;
-      const int np = mpsi[e];
       float acc[VEC];
 #pragma unroll
       for (int q = 0; q < VEC; ++q) acc[q] = 0.f;
-      for (int t = 0; t < np; ++t) {
-        const int c = mchunk[e * a.delta + t];
-        if (c < 0) continue;
-        for (int k = 0; k < a.ell; ++k) {
-          const float w = mcoef[e * stride_row + t * a.ell + k];
-          float g[VEC];
-          load_vec<GT, VEC>(Gs + (size_t(c) * a.ell + k) * W + lane * VEC, g);
+      const int32_t *ro = moff + size_t(e) * SR;
+      const float *rc = mcoef + size_t(e) * SR;
+      for (int u = 0; u < nt; u += 4) {
+        const int4 o = *reinterpret_cast<const int4 *>(ro + u);
+        const float4 cw = *reinterpret_cast<const float4 *>(rc + u);
+        float g0v[VEC], g1v[VEC], g2v[VEC], g3v[VEC];
+        load_vec<GT, VEC>(Gs + o.x + lane * VEC, g0v);
+        load_vec<GT, VEC>(Gs + o.y + lane * VEC, g1v);
+        load_vec<GT, VEC>(Gs + o.z + lane * VEC, g2v);
+        load_vec<GT, VEC>(Gs + o.w + lane * VEC, g3v);
 #pragma unroll
-          for (int q = 0; q < VEC; ++q) acc[q] = fmaf(w, g[q], acc[q]);
+        for (int q = 0; q < VEC; ++q) {
+          acc[q] = fmaf(cw.x, g0v[q], acc[q]);
+          acc[q] = fmaf(cw.y, g1v[q], acc[q]);
+          acc[q] = fmaf(cw.z, g2v[q], acc[q]);
+          acc[q] = fmaf(cw.w, g3v[q], acc[q]);
         }
       }
       if (xl < a.L) store_vec<VEC>(a.T + r * a.L + xl, acc);
@@ -887,23 +916,27 @@ template <typename GT, int VEC>
 int launch_encode(EncodeArgs a, hipStream_t st) {
   constexpr int W = kWave * VEC;
   a.nslices = int(ceil_div(a.L, W));
-  const size_t gbytes = (size_t(a.N) * a.ell * W * sizeof(GT) + 15) & ~size_t(15);
-  const size_t per_row = sizeof(int32_t) * (1 + a.delta) + sizeof(float) * a.delta * a.ell;
+  a.term_stride = (a.delta * a.ell + 3) & ~3;
+  const size_t gbytes = size_t(a.N * a.ell + 1) * W * sizeof(GT);
+  const size_t per_row = sizeof(int32_t) + (sizeof(int32_t) + sizeof(float)) * a.term_stride;
   int group = int(kEncMetaLds / per_row);
-  if (group > kEncMaxGroup) group = kEncMaxGroup;
+  if (group > kEncGroup) group = kEncGroup;
   if (group < 1) group = 1;
-  a.group_rows = group;
-  // at most kEncRowsPerBlock rows per block, and a grid that is a whole number of rounds of
-  // the blocks the chip holds at once (two per CU), so no round runs partly empty
-  const int64_t conc = 2 * int64_t(cu_count());
-  int64_t gg = a.nslices, h = conc;
-  while (h) { const int64_t t = gg % h; gg = h; h = t; }
-  const int64_t step = conc / gg;  // row blocks per round of the grid
-  const int64_t rblocks = ceil_div(ceil_div(a.rows, kEncRowsPerBlock), step) * step;
+  // runs of a few hundred rows: long enough to amortise the slice staging, short enough
+  // that the blocks in flight keep a compact write front (longer only where the grid
+  // would otherwise exceed the launch limits)
+  const int64_t max_blocks = 0xffffffffLL / kEncThreads;
+  int64_t rblocks = ceil_div(a.rows, int64_t(group) * kEncGroupsPerBlock);
+  if (rblocks * a.nslices > max_blocks) rblocks = max_blocks / a.nslices;
+  if (rblocks < 1) return GC_EINVAL;
   a.rows_per_block = ceil_div(a.rows, rblocks);
+  if (a.rows_per_block < group) group = int(a.rows_per_block);
+  a.group_rows = group;
+  rblocks = ceil_div(a.rows, a.rows_per_block);
   const int64_t blocks = rblocks * a.nslices;
   if (!grid_ok(blocks, kEncThreads)) return GC_EINVAL;
-  const size_t lds = gbytes + per_row * group;
+  const size_t lds = gbytes + sizeof(int32_t) * ((group + 3) & ~3) +
+                     (sizeof(int32_t) + sizeof(float)) * a.term_stride * size_t(group);
   if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_kernel<GT, VEC>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
     return GC_ELAUNCH;
