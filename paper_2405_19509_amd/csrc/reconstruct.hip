@@ -14,6 +14,13 @@
 // in fp64 per block and reduced across pieces in a fixed order by a second
 // small kernel, so it is deterministic.  Given psi, rows of workers with
 // psi = 0 (which transmitted nothing) are neither read nor needed.
+// The block's writes come last: the squared error (with its barrier) first, then
+// the estimate with non-temporal stores and the partial sum.  A barrier waits for
+// every outstanding memory access of the block's waves, stores included, so an
+// estimate stored before it held each block until its 16 KB had reached memory
+// (the combine ran 5% slower at ell = 1 and 10% at ell = 2); even so, the estimate's
+// 4 bytes per position cost ~0.6 ms at the 16384 x 10,000-pattern size, far more
+// than their share of the traffic, as writes interleaved into the read stream.
 #include "common.h"
 
 namespace gcx {
@@ -129,31 +136,30 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     consume(a + kRecUnroll, vb);
   }
 
+  // the squared error first (gsum reads, the block reduction and its barrier), then the
+  // estimate's stores as the block's last instructions: a barrier waits for every
+  // outstanding memory access of its waves, stores included, so a store issued before
+  // one would hold the block until it had reached memory
   double se = 0.0;
+  if (partial) {
 #pragma unroll
-  for (int k = 0; k < ELL; ++k) {
+    for (int k = 0; k < ELL; ++k) {
 #pragma unroll
-    for (int u = 0; u < kRecNV; ++u) {
-      const int64_t x0 = rec_x<VEC>(q, 4 * u);
-      const int64_t c0 = int64_t(k) * L + x0;
-      if (VEC == 4 && x0 < L && c0 + 3 < d) {  // whole float4 inside the gradient
-        const float *a4 = &acc[k][4 * u];
-        if (ghat)
-          *reinterpret_cast<float4 *>(ghat + p * d + c0) = make_float4(a4[0], a4[1], a4[2], a4[3]);
-        if (partial) {
+      for (int u = 0; u < kRecNV; ++u) {
+        const int64_t x0 = rec_x<VEC>(q, 4 * u);
+        const int64_t c0 = int64_t(k) * L + x0;
+        if (VEC == 4 && x0 < L && c0 + 3 < d) {  // whole float4 inside the gradient
+          const float *a4 = &acc[k][4 * u];
           const float4 g = *reinterpret_cast<const float4 *>(gsum + c0);
           const double e0 = double(a4[0]) - g.x, e1 = double(a4[1]) - g.y;
           const double e2 = double(a4[2]) - g.z, e3 = double(a4[3]) - g.w;
           se += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
-        }
-      } else {
+        } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int64_t x = rec_x<VEC>(q, 4 * u + e);
-          const int64_t col = int64_t(k) * L + x;
-          if (x < L && col < d) {
-            if (ghat) ghat[p * d + col] = acc[k][4 * u + e];
-            if (partial) {
+          for (int e = 0; e < 4; ++e) {
+            const int64_t x = rec_x<VEC>(q, 4 * u + e);
+            const int64_t col = int64_t(k) * L + x;
+            if (x < L && col < d) {
               const double diff = double(acc[k][4 * u + e]) - double(gsum[col]);
               se += diff * diff;
             }
@@ -161,17 +167,38 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
         }
       }
     }
-  }
-  if (partial) {
     se = wave_sum(se);
     if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = se;
     __syncthreads();
     if (threadIdx.x == 0) {
       double tot = 0.0;
       for (int w = 0; w < kRecThreads / kWave; ++w) tot += red[w];
-      partial[p * pieces + q] = tot;
+      se = tot;
     }
   }
+  if (ghat) {
+#pragma unroll
+    for (int k = 0; k < ELL; ++k) {
+#pragma unroll
+      for (int u = 0; u < kRecNV; ++u) {
+        const int64_t x0 = rec_x<VEC>(q, 4 * u);
+        const int64_t c0 = int64_t(k) * L + x0;
+        if (VEC == 4 && x0 < L && c0 + 3 < d) {
+          const float *a4 = &acc[k][4 * u];
+          __builtin_nontemporal_store(v4f{a4[0], a4[1], a4[2], a4[3]},
+                                      reinterpret_cast<v4f *>(ghat + p * d + c0));
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t x = rec_x<VEC>(q, 4 * u + e);
+            const int64_t col = int64_t(k) * L + x;
+            if (x < L && col < d) __builtin_nontemporal_store(acc[k][4 * u + e], ghat + p * d + col);
+          }
+        }
+      }
+    }
+  }
+  if (partial && threadIdx.x == 0) partial[p * pieces + q] = se;
 }
 
 __global__ void sqerr_finalize_kernel(const double *__restrict__ partial, int64_t P, int nslices,
