@@ -62,12 +62,21 @@ class GcxError(RuntimeError):
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libgcx.so (once).  Raises if it has not been built."""
+    """Load libgcx.so (once).  Raises if it has not been built.
+
+    torch is imported first: the PyTorch ROCm wheel ships its own HIP runtime, and the
+    library must bind to that one (the one that owns torch's memory and streams).  Loaded
+    before torch, libgcx.so would pull in the system HIP runtime and torch would then load
+    its own, two runtimes in one process, and launches on torch's streams would fail."""
     global _lib
     if _lib is not None:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with `python -m paper_2405_19509_amd.build`")
+    try:
+        import torch  # noqa: F401  (see above: before the library, for its HIP runtime)
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     for name, (res, args) in SIGNATURES.items():
         f = getattr(lib, name)

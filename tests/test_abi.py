@@ -211,3 +211,18 @@ def test_qmax_matches_the_oracle():
     bad[0, 0] = 2                                  # two chunks at position 2 of worker 0
     with pytest.raises(gcx.GcxError):
         gcx.gc_qmax(bad)
+
+
+def test_binding_shares_torchs_hip_runtime():
+    """The binding loads libgcx.so after torch, so a process holds one HIP runtime (the
+    one torch ships): loaded first, the library pulls in the system runtime and torch then
+    maps its own next to it, and launches on torch's streams fail."""
+    import subprocess
+    import sys
+    code = ("from paper_2405_19509_amd import gcx; gcx.load(); import torch; "
+            "maps = open('/proc/self/maps').read().splitlines(); "
+            "print(len({l.split()[-1] for l in maps if 'libamdhip64' in l}))")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1"
