@@ -294,9 +294,16 @@ MR_WL_BF16 = Workload(name="mr_m200_d4001_bf16", N=200, m=200, s=19, d=4001, P=3
 MR_CASES = [(MR_WL, 2, 1), (MR_WL, 2, 2), (MR_WL, 2, 7), (MR_WL, 2, 16), (MR_WL_BF16, 4, 3)]
 
 
-def _encode_against_oracle(O, order, psi, R, G, g_dtype, ell, d):
+def _encode_against_oracle(O, order, psi, R, G, g_dtype, ell, d, shift=0):
+    """The encode of G (placed `shift` elements past an aligned device allocation) against
+    the oracle's, on the oracle's coefficients rounded to fp32."""
     Bc32 = R_.coefficients(O, psi, R)[0].astype(np.float32)
     Gt = dev(G.view(np.int16)).view(torch.bfloat16) if g_dtype == "bf16" else dev(G)
+    if shift:
+        buf = torch.empty(Gt.numel() + shift, dtype=Gt.dtype, device="cuda")
+        moved = buf[shift:].view(Gt.shape)
+        moved.copy_(Gt)
+        Gt = moved
     Td = torch.full((len(psi), O.shape[1], -(-d // ell)), float("nan"), device="cuda")
     T = host(gcx.gc_encode(Gt, dev(psi), dev(order), dev(Bc32), T=Td))
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, g_dtype), ell)
@@ -304,6 +311,20 @@ def _encode_against_oracle(O, order, psi, R, G, g_dtype, ell, d):
     assert np.isnan(T[~sent]).all()
     bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
+
+
+@pytest.mark.parametrize("ell", [1, 2])
+@pytest.mark.parametrize("g_dtype,shift", [("f32", 0), ("f32", 1), ("bf16", 0), ("bf16", 1)])
+def test_encode_all_chunk_staging(g_dtype, shift, ell):
+    """The all-chunk layout with its slices staged straight into LDS 16 bytes at a time (G
+    16-byte aligned, d and L whole 16-byte pieces), and element by element when G sits one
+    element off that alignment; 23 x 40 = 920 rows: two 256-row metadata groups in the first
+    block, a ragged second block."""
+    wl = Workload(name=f"allchunk_m40_d4096_{g_dtype}", N=40, m=40, s=3, d=4096, P=23, ells=(ell,),
+                  g_dtype=g_dtype, pattern="uniform")
+    O, order, _, _ = tables(wl)
+    _encode_against_oracle(O, order, patterns(wl, 23), gen.shared_R(wl.m, ell), given_G(wl), g_dtype,
+                           ell, wl.d, shift=shift)
 
 
 @pytest.mark.parametrize("wl,ell,count", MR_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in MR_CASES])
