@@ -3,9 +3,10 @@
 // target; and gc_sum_chunks, the exact target sum_i g_{D_i} itself.
 //
 // Bandwidth design (HBM-bound on the T read, ~0.5 flop per byte): a block of
-// 1024 threads owns one pattern and one piece of 4096 consecutive x positions
-// (16 KB of every transmitting worker's row, read as one coalesced sweep per
-// row); consecutive blocks take consecutive pieces of a pattern.  Measured on
+// 1024 threads takes items, each one pattern and one piece of 4096 consecutive x
+// positions (16 KB of every transmitting worker's row, read as one coalesced sweep
+// per row); consecutive items are consecutive pieces of a pattern, and a block
+// takes up to 8 / ell consecutive items when the estimate is written (see below).  Measured on
 // MI355X, 16 KB per row and block beats 4 KB and 8 KB (2-3%), and one float4
 // per thread and row beats two or four.  Each thread holds one float4 of ell
 // accumulators and keeps kRecUnroll rows of loads in flight; the transmitting
@@ -14,13 +15,15 @@
 // in fp64 per block and reduced across pieces in a fixed order by a second
 // small kernel, so it is deterministic.  Given psi, rows of workers with
 // psi = 0 (which transmitted nothing) are neither read nor needed.
-// The block's writes come last: the squared error (with its barrier) first, then
-// the estimate with non-temporal stores and the partial sum.  A barrier waits for
-// every outstanding memory access of the block's waves, stores included, so an
-// estimate stored before it held each block until its 16 KB had reached memory
-// (the combine ran 5% slower at ell = 1 and 10% at ell = 2); even so, the estimate's
-// 4 bytes per position cost ~0.6 ms at the 16384 x 10,000-pattern size, far more
-// than their share of the traffic, as writes interleaved into the read stream.
+// The block's writes come last: every item's squared error (with its barrier) first,
+// then the estimates with non-temporal stores and the partial sums.  A barrier waits
+// for every outstanding memory access of the block's waves, stores included, so an
+// estimate stored before one held the block until it had reached memory (the combine
+// ran 5% slower at ell = 1 and 10% at ell = 2).  The estimate's 4 bytes per position,
+// interleaved into the read stream, still cost far more than their share of the
+// traffic (~0.6 ms at the 16384 x 10,000-pattern size with one 16 KB write per item);
+// written in 128 KB bursts, 8 / ell items' worth held in LDS per block, they cost
+// about a third less.
 #include "common.h"
 
 namespace gcx {
@@ -68,38 +71,88 @@ __device__ __forceinline__ void rec_load(const float *__restrict__ row, int64_t 
   }
 }
 
+// Items per block when the estimate is written: K consecutive (pattern, piece) items,
+// each item's estimate held in LDS (ell * 16 KB) and all K written at the block's end.
+// Interleaved into the read stream, the estimate's writes cost far more than their bytes;
+// 128 KB bursts per block cost a third less than one 16 KB write per item.
+template <int ELL>
+constexpr int rec_items() { return ELL == 1 ? 8 : (ELL == 2 ? 4 : (ELL <= 4 ? 2 : 1)); }
+
+// the estimate's stores of one item (positions as rec_x; the whole float4 where it lies
+// inside the gradient, else element by element)
 template <int ELL, int VEC>
+__device__ __forceinline__ void rec_store(float *__restrict__ ghat, int64_t p, int64_t q, int64_t d,
+                                          int64_t L, const float (&acc)[ELL][kRecV]) {
+#pragma unroll
+  for (int k = 0; k < ELL; ++k) {
+#pragma unroll
+    for (int u = 0; u < kRecNV; ++u) {
+      const int64_t x0 = rec_x<VEC>(q, 4 * u);
+      const int64_t c0 = int64_t(k) * L + x0;
+      if (VEC == 4 && x0 < L && c0 + 3 < d) {
+        const float *a4 = &acc[k][4 * u];
+        __builtin_nontemporal_store(v4f{a4[0], a4[1], a4[2], a4[3]},
+                                    reinterpret_cast<v4f *>(ghat + p * d + c0));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t x = rec_x<VEC>(q, 4 * u + e);
+          const int64_t col = int64_t(k) * L + x;
+          if (x < L && col < d) __builtin_nontemporal_store(acc[k][4 * u + e], ghat + p * d + col);
+        }
+      }
+    }
+  }
+}
+
+// K items per block: item it = blockIdx.x * K + i (pattern it / pieces, piece it % pieces).
+// With K > 1 the estimates wait in LDS (`held`, K * ELL * 16 KB of dynamic LDS) and the
+// partial sums in `part_s` until every item is done: a barrier waits for every
+// outstanding memory access of the block's waves, stores included, so the block's stores
+// all come after its last barrier.
+template <int ELL, int VEC, int K>
 __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     const float *__restrict__ T, const float *__restrict__ R, const int32_t *__restrict__ psi,
-    int m, int64_t d, int64_t L, int64_t pieces, float *__restrict__ ghat,
+    int m, int64_t d, int64_t L, int64_t pieces, int64_t items, float *__restrict__ ghat,
     const float *__restrict__ gsum, double *__restrict__ partial) {
   __shared__ double red[kRecThreads / kWave];
+  __shared__ double part_s[K];
   __shared__ int rows[GC_MAX_M];      // the workers that transmitted, ascending
   __shared__ float rw[ELL][GC_MAX_M];  // their R[k][j]
   __shared__ int nrows;
-  const int64_t p = blockIdx.x / pieces;
-  const int64_t q = blockIdx.x % pieces;
+  extern __shared__ __align__(16) unsigned char rec_dyn[];
+  v4f *held = reinterpret_cast<v4f *>(rec_dyn);  // [K][ELL][kRecThreads] (K > 1)
+  const int64_t it0 = int64_t(blockIdx.x) * K;
+  const int nit = int(items - it0 < K ? items - it0 : K);
+  int64_t cur_p = -1;
+  for (int item = 0; item < nit; ++item) {
+  const int64_t p = (it0 + item) / pieces;
+  const int64_t q = (it0 + item) % pieces;
   const float *Tp = T + p * int64_t(m) * L;
+  __syncthreads();  // the previous item's rows, weights and reduction slots are free
 
   // compact the transmitting workers (psi > 0) with ballots in wave 0, with their
   // weights R[k][j]; with no psi every worker counts as transmitting
-  if (threadIdx.x < kWave) {
-    int cnt = 0;
-    for (int base = 0; base < m; base += kWave) {
-      const int j = base + int(threadIdx.x);
-      const bool on = j < m && (psi == nullptr || psi[p * m + j] > 0);
-      const unsigned long long mask = __ballot(on);
-      if (on) {
-        const int a = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
-        rows[a] = j;
+  if (p != cur_p) {
+    if (threadIdx.x < kWave) {
+      int cnt = 0;
+      for (int base = 0; base < m; base += kWave) {
+        const int j = base + int(threadIdx.x);
+        const bool on = j < m && (psi == nullptr || psi[p * m + j] > 0);
+        const unsigned long long mask = __ballot(on);
+        if (on) {
+          const int a = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
+          rows[a] = j;
 #pragma unroll
-        for (int k = 0; k < ELL; ++k) rw[k][a] = R[int64_t(k) * m + j];
+          for (int k = 0; k < ELL; ++k) rw[k][a] = R[int64_t(k) * m + j];
+        }
+        cnt += __popcll(mask);
       }
-      cnt += __popcll(mask);
+      if (threadIdx.x == 0) nrows = cnt;
     }
-    if (threadIdx.x == 0) nrows = cnt;
+    __syncthreads();
+    cur_p = p;
   }
-  __syncthreads();
   const int nr = nrows;
 
   float acc[ELL][kRecV];
@@ -107,7 +160,6 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
   for (int k = 0; k < ELL; ++k)
 #pragma unroll
     for (int i = 0; i < kRecV; ++i) acc[k][i] = 0.f;
-
   // software pipeline: the loads of the next kRecUnroll rows are in flight while the
   // current ones are consumed
   float va[kRecUnroll][kRecV], vb[kRecUnroll][kRecV];
@@ -136,12 +188,9 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     consume(a + kRecUnroll, vb);
   }
 
-  // the squared error first (gsum reads, the block reduction and its barrier), then the
-  // estimate's stores as the block's last instructions: a barrier waits for every
-  // outstanding memory access of its waves, stores included, so a store issued before
-  // one would hold the block until it had reached memory
-  double se = 0.0;
+  // the squared error (gsum reads, the block reduction and its barrier) of this item
   if (partial) {
+    double se = 0.0;
 #pragma unroll
     for (int k = 0; k < ELL; ++k) {
 #pragma unroll
@@ -173,32 +222,34 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
     if (threadIdx.x == 0) {
       double tot = 0.0;
       for (int w = 0; w < kRecThreads / kWave; ++w) tot += red[w];
-      se = tot;
+      part_s[item] = tot;
     }
   }
-  if (ghat) {
+  if constexpr (K == 1) {
+    // one item: nothing follows, so its stores can go out directly
+    if (ghat) rec_store<ELL, VEC>(ghat, p, q, d, L, acc);
+  } else {
 #pragma unroll
-    for (int k = 0; k < ELL; ++k) {
+    for (int k = 0; k < ELL; ++k)
+      held[(item * ELL + k) * kRecThreads + threadIdx.x] = v4f{acc[k][0], acc[k][1], acc[k][2], acc[k][3]};
+  }
+  }  // items
+
+  // the block's stores, after its last barrier
+  if constexpr (K > 1) {
+    for (int item = 0; item < nit; ++item) {
+      const int64_t p = (it0 + item) / pieces, q = (it0 + item) % pieces;
+      float acc[ELL][kRecV];
 #pragma unroll
-      for (int u = 0; u < kRecNV; ++u) {
-        const int64_t x0 = rec_x<VEC>(q, 4 * u);
-        const int64_t c0 = int64_t(k) * L + x0;
-        if (VEC == 4 && x0 < L && c0 + 3 < d) {
-          const float *a4 = &acc[k][4 * u];
-          __builtin_nontemporal_store(v4f{a4[0], a4[1], a4[2], a4[3]},
-                                      reinterpret_cast<v4f *>(ghat + p * d + c0));
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int64_t x = rec_x<VEC>(q, 4 * u + e);
-            const int64_t col = int64_t(k) * L + x;
-            if (x < L && col < d) __builtin_nontemporal_store(acc[k][4 * u + e], ghat + p * d + col);
-          }
-        }
+      for (int k = 0; k < ELL; ++k) {
+        const v4f h = held[(item * ELL + k) * kRecThreads + threadIdx.x];
+        acc[k][0] = h.x; acc[k][1] = h.y; acc[k][2] = h.z; acc[k][3] = h.w;
       }
+      rec_store<ELL, VEC>(ghat, p, q, d, L, acc);
     }
   }
-  if (partial && threadIdx.x == 0) partial[p * pieces + q] = se;
+  if (partial && threadIdx.x == 0)
+    for (int item = 0; item < nit; ++item) partial[it0 + item] = part_s[item];
 }
 
 __global__ void sqerr_finalize_kernel(const double *__restrict__ partial, int64_t P, int nslices,
@@ -210,17 +261,33 @@ __global__ void sqerr_finalize_kernel(const double *__restrict__ partial, int64_
   sqerr[p] = tot;
 }
 
+template <int ELL, int VEC, int K>
+int launch_rec_k(const float *T, const float *R, const int32_t *psi, int64_t P, int m, int64_t d,
+                 int64_t L, int64_t pieces, float *ghat, const float *gsum, double *partial,
+                 hipStream_t st) {
+  const int64_t items = P * pieces;
+  const int64_t blocks = ceil_div(items, int64_t(K));
+  if (!grid_ok(blocks, kRecThreads)) return GC_EINVAL;
+  const size_t dyn = K > 1 ? sizeof(v4f) * size_t(K) * ELL * kRecThreads : 0;
+  if (dyn > 0 && hipFuncSetAttribute(reinterpret_cast<const void *>(&reconstruct_kernel<ELL, VEC, K>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, int(dyn)) != hipSuccess)
+    return GC_ELAUNCH;
+  hipLaunchKernelGGL((reconstruct_kernel<ELL, VEC, K>), dim3(unsigned(blocks)), dim3(kRecThreads), dyn, st,
+                     T, R, psi, m, d, L, pieces, items, ghat, gsum, partial);
+  return GC_OK;
+}
+
+// items per block: rec_items<ELL>() when the estimate is written, else one
 template <int ELL>
-void launch_rec(bool vec4, const float *T, const float *R, const int32_t *psi, int64_t P, int m,
-                int64_t d, int64_t L, int64_t pieces, float *ghat, const float *gsum, double *partial,
-                hipStream_t st) {
-  const dim3 grid(unsigned(P * pieces));
-  if (vec4)
-    hipLaunchKernelGGL((reconstruct_kernel<ELL, 4>), grid, dim3(kRecThreads), 0, st, T, R, psi, m, d,
-                       L, pieces, ghat, gsum, partial);
-  else
-    hipLaunchKernelGGL((reconstruct_kernel<ELL, 1>), grid, dim3(kRecThreads), 0, st, T, R, psi, m, d,
-                       L, pieces, ghat, gsum, partial);
+int launch_rec(bool vec4, const float *T, const float *R, const int32_t *psi, int64_t P, int m,
+               int64_t d, int64_t L, int64_t pieces, float *ghat, const float *gsum, double *partial,
+               hipStream_t st) {
+  constexpr int KB = rec_items<ELL>();
+  if (ghat && KB > 1)
+    return vec4 ? launch_rec_k<ELL, 4, KB>(T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, st)
+                : launch_rec_k<ELL, 1, KB>(T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, st);
+  return vec4 ? launch_rec_k<ELL, 4, 1>(T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, st)
+              : launch_rec_k<ELL, 1, 1>(T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, st);
 }
 
 __global__ void sum_chunks_kernel(const void *__restrict__ G, int bf16, int N, int64_t d,
@@ -277,15 +344,17 @@ extern "C" int gc_reconstruct(const float *T, const float *R, const int32_t *psi
   const bool vec4 = L % 4 == 0 && d % 4 == 0 && aligned16(T) && (!ghat || aligned16(ghat)) &&
                     (!gsum || aligned16(gsum));
   (void)hipGetLastError();
+  int st = GC_OK;
   switch (ell) {
 #define GC_CASE(E)                                                                           \
   case E:                                                                                    \
-    launch_rec<E>(vec4, T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, stream);         \
+    st = launch_rec<E>(vec4, T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, stream);    \
     break;
     GC_CASE(1) GC_CASE(2) GC_CASE(3) GC_CASE(4) GC_CASE(5) GC_CASE(6) GC_CASE(7) GC_CASE(8)
 #undef GC_CASE
     default: return GC_EINVAL;
   }
+  if (st != GC_OK) return st;
   if (want_err && pieces > 1)
     hipLaunchKernelGGL(sqerr_finalize_kernel, dim3(unsigned(ceil_div(P, 256))), dim3(256), 0,
                        stream, partial, P, int(pieces), sqerr);
