@@ -16,7 +16,7 @@
 //     row: fully coalesced, and every T byte is written exactly once;
 //   - the run length trades the slice staging (N*ell*W values per block, from
 //     L2) against the spread of the write front: the blocks in flight cover
-//     every slice of a few thousand rows, and runs of ~512 rows wrote T ~5%
+//     every slice of a few thousand rows, and runs of ~512 rows wrote T ~4%
 //     faster than runs of 4096 (runs of 64-128 lose more to the per-block
 //     staging and latency than they gain);
 //   - block -> (slice, row run) is XCD-aware: blocks are dispatched round-robin

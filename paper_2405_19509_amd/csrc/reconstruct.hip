@@ -6,9 +6,9 @@
 // 1024 threads takes items, each one pattern and one piece of 4096 consecutive x
 // positions (16 KB of every transmitting worker's row, read as one coalesced sweep
 // per row); consecutive items are consecutive pieces of a pattern, and a block
-// takes up to 8 / ell consecutive items when the estimate is written (see below).  Measured on
-// MI355X, 16 KB per row and block beats 4 KB and 8 KB (2-3%), and one float4
-// per thread and row beats two or four.  Each thread holds one float4 of ell
+// takes several consecutive items when the estimate is written (see below).
+// Measured on MI355X, 16 KB per row and item beats 4 KB and 8 KB (2-3%), and one
+// float4 per thread and row beats two or four.  Each thread holds one float4 of ell
 // accumulators and keeps kRecUnroll rows of loads in flight; the transmitting
 // rows and their weights R[k][j] are compacted into LDS first.  T is read with
 // non-temporal loads (it is consumed once).  The squared error is accumulated
