@@ -234,6 +234,42 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     assert (host(sq2) == sqerr).all()
 
 
+def test_encode_and_reconstruct_edge_patterns():
+    """No worker done (nothing transmitted: the estimate is 0 and the squared error |gsum|^2),
+    all done, a single worker done, one chunk each, all but the last chunk; the combine takes
+    several items per block at ell = 1 and 2 (one with no transmitting row) and one at ell = 8."""
+    wl = dataclasses.replace(TINY, name="tiny_edges_ec")
+    m, delta = wl.m, wl.delta
+    psi = np.array([[0] * m, [delta] * m, [delta] + [0] * (m - 1), [1] * m, [delta - 1] * m],
+                   dtype=np.int32)
+    O, order, _, _ = tables(wl)
+    G = _data_G(wl)
+    Gw = OP.widen(G, wl.g_dtype)
+    gsum32 = Gw.sum(axis=0).astype(np.float32)
+    sent = psi > 0
+    for ell in (1, 2, 8):
+        R = gen.shared_R(m, ell)
+        Bc32 = R_.coefficients(O, psi, R)[0].astype(np.float32)
+        Td = torch.full((len(psi), m, -(-wl.d // ell)), float("nan"), device="cuda")
+        T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32), T=Td))
+        T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, Gw, ell)
+        assert np.isnan(T[~sent]).all()
+        bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+        assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
+        T32 = T_ref.astype(np.float32)  # rows of workers with psi = 0 are zero in the oracle's T
+        T32_poison = T32.copy()
+        T32_poison[~sent] = np.nan
+        ghat, sq = gcx.gc_reconstruct(dev(T32_poison), dev(R), wl.d, psi=dev(psi), gsum=dev(gsum32))
+        ghat, sq = host(ghat), host(sq)
+        assert (ghat[0] == 0).all()
+        assert sq[0] == pytest.approx(float((gsum32.astype(np.float64) ** 2).sum()), rel=1e-12)
+        gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, wl.d)
+        assert (np.abs(ghat.astype(np.float64) - gh_ref) <= R_.gamma(m) * mag).all()
+        se_ref = ((gh_ref - gsum32.astype(np.float64)) ** 2).sum(axis=1)
+        E = np.sqrt(((R_.gamma(m) * mag) ** 2).sum(axis=1))
+        assert (np.abs(sq - se_ref) <= 2 * np.sqrt(se_ref) * E + E * E + 1e-12 * se_ref).all()
+
+
 # worker-group encode layout: many chunks per slice, so the all-chunk layout does not fit;
 # odd L (one float per lane), padding (ell does not divide d), bf16, 1 to 7 patterns per call
 GROUP_CASES = [
