@@ -548,8 +548,9 @@ def main():
             e1.record()
             torch.cuda.synchronize()
             probe[key + "_GBps"] = nbytes / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
-        probe["note"] = ("gc_hbm_probe: one 4 KB piece per block, blocks in order, non-temporal "
-                         "16-byte stores / loads over the same number of bytes as the encode's T")
+        probe["note"] = ("gc_hbm_probe: one 4 KB piece per block, blocks in order, 16-byte "
+                         "system-scope (sc1) stores / non-temporal loads over the same number of "
+                         "bytes as the encode's T")
 
     for _ in range(args.warmup):
         step()
