@@ -51,8 +51,6 @@ def parse():
     ap.add_argument("--mfma-points", type=int, default=256,
                     help="also time the chunk gradients at this many evaluation points (matrix-core "
                          "path; 0 = skip); reported under 'mfma', outside the step")
-    ap.add_argument("--no-hbm-probe", dest="hbm_probe", action="store_false",
-                    help="skip the plain write/read streams that calibrate the HBM-bound kernels")
     ap.add_argument("--no-decode-large", dest="decode_large", action="store_false",
                     help="skip timing the coefficients of the 100,000-pattern m = 200 workload "
                          "(reported under 'decode_large', outside the step)")
@@ -532,26 +530,6 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # what the HBM delivers here for plain streams of the encode's T bytes (calibration)
-    probe = None
-    if args.hbm_probe:
-        nbytes = int((psi > 0).sum()) * L * 4
-        sink = torch.zeros(1, dtype=torch.float32, device=dev)
-        probe = {"bytes": nbytes}
-        for mode, key in ((0, "write"), (1, "read")):
-            gcx.gc_hbm_probe(T, nbytes, mode, sink)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(5):
-                gcx.gc_hbm_probe(T, nbytes, mode, sink)
-            e1.record()
-            torch.cuda.synchronize()
-            probe[key + "_GBps"] = nbytes / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
-        probe["note"] = ("gc_hbm_probe: one 4 KB piece per block, blocks in order, 16-byte "
-                         "system-scope (sc1) stores / non-temporal loads over the same number of "
-                         "bytes as the encode's T")
-
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -592,10 +570,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(wl, dominant) if ell == 1 else None,
-                     "algorithmic_bytes": nbytes[dominant], "avg_ms": avg_ms[dominant],
-                     "frac_of_probe": (achieved / probe["write_GBps" if dominant == "gc_encode" else "read_GBps"]
-                                       if probe else None)},
-        "hbm_probe": probe,
+                     "algorithmic_bytes": nbytes[dominant], "avg_ms": avg_ms[dominant]},
         "kernels_ms": avg_ms,
         "kernels_gbs": gbs,
         "decoded_gradients_per_s": float((decs == 1).sum()) * args.steps / elapsed,

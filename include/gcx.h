@@ -204,8 +204,9 @@ int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_
  * gc_reconstruct -- the PS combine (Sec. 2.2, last step): block k of the
  * estimate is sum_j R[k][j] T[p][j][:] over the workers that transmitted, i.e.
  *   ghat[p][k*L + x] = sum_{j : psi[p][j] > 0} R[k][j] * T[p][j][x]   for k*L + x < d.
- * psi [P][m] int32 device, or NULL to combine every row of T (then rows of
- * non-transmitting workers must hold zeros).  Rows with psi <= 0 are not read.
+ * psi [P][m] int32 device, required (GC_EINVAL if NULL): it names the workers
+ * that transmitted, and rows of T with psi <= 0 are never read, so the T that
+ * gc_encode leaves unwritten for stragglers is combined correctly.
  * Equals sum_i g_{D_i} when the pattern is decodable; otherwise it is the
  * least-squares estimate.  If gsum is non-NULL and sqerr non-NULL,
  *   sqerr[p] = sum_x (ghat[p][x] - gsum[x])^2   (fp64 accumulation)
@@ -293,16 +294,6 @@ int gc_completion_times(const double *tau, const uint8_t *failed, int64_t R, int
 int gc_original_ls(const int32_t *psi, int64_t P, int32_t N, int32_t m, const int32_t *order,
                    int32_t delta, const int32_t *holder, int32_t gamma, int32_t max_iter,
                    double tol, double *err, int32_t *iters, hipStream_t stream);
-
-/*
- * gc_hbm_probe -- calibration, not a step of the method: streams over `bytes`
- * bytes of buf (device, 16-byte aligned) with one 4 KB piece per block, blocks
- * in order, writing constants (mode 0, non-temporal 16-byte stores) or reading
- * (mode 1, non-temporal 16-byte loads; sink: one device float, written only for
- * a value finite data never produce).  Timing it gives the streaming bandwidth
- * this device delivers, the practical ceiling of the HBM-bound kernels.
- */
-int gc_hbm_probe(void *buf, size_t bytes, int32_t mode, float *sink, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -39,13 +39,3 @@ def chunk_gradients(X: np.ndarray, y: np.ndarray, W: np.ndarray, loss: str) -> n
         return np.stack([chunk_gradient(X[i], y[i], W, loss) for i in range(X.shape[0])])
     return np.stack([chunk_gradients(X, y, W[q], loss) for q in range(W.shape[0])])
 
-
-def loss_value(X: np.ndarray, y: np.ndarray, w: np.ndarray, loss: str) -> float:
-    """sum over all samples of l(x, y, w) (no normalisation), fp64."""
-    X = np.asarray(X, dtype=np.float64).reshape(-1, X.shape[-1])
-    y = np.asarray(y, dtype=np.float64).reshape(-1)
-    z = X @ np.asarray(w, dtype=np.float64)
-    if loss == "linear":
-        return float(0.5 * np.sum((z - y) ** 2))
-    # -y log s(z) - (1-y) log(1-s(z)) = log(1 + e^z) - y z
-    return float(np.sum(np.logaddexp(0.0, z) - y * z))

@@ -132,13 +132,13 @@ __global__ __launch_bounds__(kRecThreads) void reconstruct_kernel(
   __syncthreads();  // the previous item's rows, weights and reduction slots are free
 
   // compact the transmitting workers (psi > 0) with ballots in wave 0, with their
-  // weights R[k][j]; with no psi every worker counts as transmitting
+  // weights R[k][j]
   if (p != cur_p) {
     if (threadIdx.x < kWave) {
       int cnt = 0;
       for (int base = 0; base < m; base += kWave) {
         const int j = base + int(threadIdx.x);
-        const bool on = j < m && (psi == nullptr || psi[p * m + j] > 0);
+        const bool on = j < m && psi[p * m + j] > 0;
         const unsigned long long mask = __ballot(on);
         if (on) {
           const int a = cnt + __popcll(mask & ((1ull << threadIdx.x) - 1));
@@ -321,7 +321,7 @@ extern "C" int gc_reconstruct(const float *T, const float *R, const int32_t *psi
   using namespace gcx;
   if (P < 0 || m < 1 || m > GC_MAX_M || d < 1 || ell < 1 || ell > GC_MAX_ELL) return GC_EINVAL;
   if (P == 0) return GC_OK;
-  if (!T || !R) return GC_EINVAL;
+  if (!T || !R || !psi) return GC_EINVAL;
   const bool want_err = sqerr != nullptr;
   if (want_err && !gsum) return GC_EINVAL;
   if (!ghat && !want_err) return GC_OK;  // nothing requested

@@ -46,7 +46,6 @@ SIGNATURES = {
     "gc_original_ls": (_c.c_int, [_p, _i64, _i32, _i32, _p, _i32, _p, _i32, _i32, _c.c_double, _p, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
-    "gc_hbm_probe": (_c.c_int, [_p, _sz, _i32, _p, _p]),
     "gc_decode_direct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_decode_direct": (_c.c_int, [_p, _i32, _i32, _i64, _p, _i64, _i32, _i32, _p, _p, _i32, _p,
                                     _i32, _p, _p, _p, _p, _sz, _p]),
@@ -263,9 +262,9 @@ def gc_reconstruct_workspace_size(P: int, m: int, d: int, ell: int) -> int:
     return int(load().gc_reconstruct_workspace_size(P, m, d, ell))
 
 
-def gc_reconstruct(T, R, d: int, psi=None, ghat=None, gsum=None, sqerr=None, want_ghat: bool = True,
+def gc_reconstruct(T, R, d: int, psi, ghat=None, gsum=None, sqerr=None, want_ghat: bool = True,
                    workspace=None, stream=None):
-    """T [P][m][L], R [ell][m], psi [P][m] (or None: combine every row) ->
+    """T [P][m][L], R [ell][m], psi [P][m] (required: rows with psi <= 0 are not read) ->
     (ghat [P][d] or None, sqerr [P] fp64 or None).  sqerr is computed when gsum [d] is given."""
     torch = _torch()
     P, m, L = T.shape
@@ -286,25 +285,13 @@ def gc_reconstruct(T, R, d: int, psi=None, ghat=None, gsum=None, sqerr=None, wan
             ws_ptr, ws_bytes = _dev(workspace, "workspace", torch.uint8), workspace.numel()
     st = load().gc_reconstruct(
         _dev(T, "T", torch.float32), _dev(R, "R", torch.float32, (ell, m)),
-        _dev(psi, "psi", torch.int32, (P, m)) if psi is not None else None, P, m, d, ell,
+        _dev(psi, "psi", torch.int32, (P, m)), P, m, d, ell,
         _dev(ghat, "ghat", torch.float32, (P, d)) if ghat is not None else None,
         _dev(gsum, "gsum", torch.float32, (d,)) if gsum is not None else None,
         _dev(sqerr, "sqerr", torch.float64, (P,)) if sqerr is not None else None,
         ws_ptr, ws_bytes, _stream(stream))
     _check("gc_reconstruct", st)
     return ghat, sqerr
-
-
-def gc_hbm_probe(buf, nbytes: int, mode: int, sink=None, stream=None):
-    """Calibration stream over the first nbytes of a device tensor: mode 0 writes, 1 reads."""
-    torch = _torch()
-    if nbytes > buf.numel() * buf.element_size():
-        raise ValueError("nbytes exceeds the buffer")
-    if mode == 1 and sink is None:
-        sink = torch.zeros(1, dtype=torch.float32, device=buf.device)
-    _check("gc_hbm_probe", load().gc_hbm_probe(buf.data_ptr(), nbytes, mode,
-                                               _dev(sink, "sink", torch.float32) if sink is not None else None,
-                                               _stream(stream)))
 
 
 def gc_decode_direct_workspace_size(P: int, N: int, d: int, ell: int) -> int:

@@ -105,7 +105,8 @@ def test_device_calls_validate_on_the_host():
     assert lib.gc_encode(p, 0, 6, 64, p, p, p, 0, 6, 3, 1, p, None) == gcx.GC_OK                # P = 0
     assert lib.gc_reconstruct(p, p, p, 4, 6, 64, 0, p, None, None, None, 0, None) == E         # ell = 0
     assert lib.gc_reconstruct(p, p, p, 4, 6, 64, 1, p, None, p, None, 0, None) == E            # sqerr w/o gsum
-    assert lib.gc_reconstruct(p, p, None, 4, 6, 1 << 20, 1, None, p, p, None, 0, None) == E    # workspace
+    assert lib.gc_reconstruct(p, p, p, 4, 6, 1 << 20, 1, None, p, p, None, 0, None) == E       # workspace
+    assert lib.gc_reconstruct(p, p, None, 4, 6, 64, 1, p, None, None, None, 0, None) == E      # null psi
     ws = gcx.gc_decode_direct_workspace_size(4, 6, 64, 1)
     args = dict(G=p, g_dtype=0, N=6, d=64, psi=p, P=4, m=6, delta=3, holder=p, hpos=p, gamma=3, R=p,
                 ell=1, ghat=p, gsum=None, sqerr=None, ws=p, ws_bytes=ws, stream=None)
@@ -119,11 +120,6 @@ def test_device_calls_validate_on_the_host():
     assert direct(ws=p + 4) == E                                        # unaligned workspace
     assert direct(holder=None) == E and direct(G=None) == E
     assert direct(P=0) == gcx.GC_OK
-    assert lib.gc_hbm_probe(None, 4096, 0, None, None) == E                                   # null
-    assert lib.gc_hbm_probe(p + 4, 4096, 0, None, None) == E                                  # unaligned
-    assert lib.gc_hbm_probe(p, 4096, 2, None, None) == E                                      # mode
-    assert lib.gc_hbm_probe(p, 4096, 1, None, None) == E                                      # read w/o sink
-    assert lib.gc_hbm_probe(p, 8, 0, None, None) == E                                         # too small
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 5, p, p, 1 << 20, None) == E                # loss
     assert lib.gc_chunk_grads(p, p, p, 2, 3, 8, 1, 0, p, p, 4, None) == E                      # small ws
     assert lib.gc_sum_chunks(p, 3, 2, 8, p, None) == E

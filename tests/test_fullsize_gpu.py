@@ -169,15 +169,30 @@ def test_bandwidth_full_size():
 
 @pytest.mark.parametrize("variant,ells", [("exact", (1, 2)), ("ls", (1, 2, 4))])
 def test_large_full_size(variant, ells):
-    """m = 200, d = 2^24, bf16 chunk gradients: coefficients for all 100,000 patterns;
-    encode + combine for single patterns at full length (13.4 GB of T at ell = 1)."""
+    """m = 200, d = 2^24, bf16 chunk gradients: coefficients for all 100,000 patterns in one
+    call (integers for every pattern, Bc on sampled patterns); encode + combine for single
+    patterns at full length (13.4 GB of T at ell = 1)."""
     wl = LARGE
     O, order, holder, hpos = tables(wl)
     psi = gen.psi(wl, variant=variant)
+    P = len(psi)
+    # coefficient rows checked against the oracle: the first patterns, both sides of the
+    # waves' first and later passes over the batch, and the last ones
+    rng = np.random.default_rng(31)
+    sample = sorted(set([0, 1, 2, 63, 64, 4095, 4096, 8191, 8192, 8193, 16383, 16384, P // 2,
+                         P - 2, P - 1] + rng.choice(P, 9, replace=False).tolist()))
+    sample_t = torch.as_tensor(sample, device="cuda")
     for ell in ells:
         R = gen.shared_R(wl.m, ell)
-        cov, dec, cerr, _ = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+        cov, dec, cerr, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
+        Bc_s = host(Bc[sample_t])
+        del Bc
         cov, dec, cerr = host(cov), host(dec), host(cerr)
+        Bc_ref, kappa = R_.coefficients(O, psi[sample], R)
+        bound = R_.bc_bound(Bc_ref, kappa, O)
+        diff = np.abs(Bc_s.astype(np.float64) - Bc_ref)
+        worst = np.unravel_index(np.argmax(diff - bound), diff.shape)
+        assert (diff <= bound).all(), f"Bc off at pattern {sample[worst[0]]}, {worst[1:]}"
         # all 100,000 patterns: coverage against the oracle's definition, vectorised over patterns
         ref = np.zeros_like(cov)
         for t in range(wl.delta):

@@ -6,8 +6,9 @@ element with the oracle:
   - coverage, decodability and coefficient error: bit-exact;
   - Bc: one fp32 rounding plus the fp64 solve's kappa^2 * 2^-53 error;
   - T and the estimate: the classical fp32 summation bound gamma_n * sum |terms|;
-  - end to end: relative L2 error of the estimate <= 1e-5 at ell = 1, and the
-    cancellation-aware bound at ell >= 2.
+  - end to end: relative L2 error of the estimate <= 1e-5 at ell = 1 and, at
+    ell >= 2, on every pattern whose matrices R[:, S_i] all have kappa_2 <= 100;
+    the other ell >= 2 patterns are held to the cancellation-aware bound.
 """
 from __future__ import annotations
 
@@ -218,9 +219,6 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     T32_poison[~sent] = np.nan
     ghat, sqerr = gcx.gc_reconstruct(dev(T32_poison), dev(R), wl.d, psi=dev(psi), gsum=dev(gsum32))
     ghat, sqerr = host(ghat), host(sqerr)
-    # without psi every row is combined; the oracle's zero rows then give the same estimate
-    ghat_all, _ = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, gsum=dev(gsum32))
-    assert np.array_equal(host(ghat_all), ghat)
     gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, wl.d)
     gb = R_.gamma(wl.m) * mag
     gdiff = np.abs(ghat.astype(np.float64) - gh_ref)
@@ -587,8 +585,13 @@ def test_end_to_end(wl, ell, count):
         allowed = np.maximum(1e-5, 4 * R_.gamma(wl.m + ell * wl.delta + 2) *
                              np.linalg.norm(mag, axis=1) / np.maximum(np.linalg.norm(gh_ref, axis=1), 1e-300))
         assert (rel <= allowed).all(), (rel / allowed).max()
+        # patterns whose every R[:, S_i] has kappa_2 <= 100 are held to the plain 1e-5
         well = kappa.max(axis=1) <= 100
-        if well.any():
-            print(f"ell={ell}: rel-L2 max {rel[well].max():.2e} over {well.sum()} patterns with kappa <= 100")
+        assert well.sum() >= len(psi) // 3, well.sum()
+        print(f"ell={ell}: rel-L2 max {rel[well].max():.2e} over {well.sum()} patterns with kappa <= 100")
+        assert rel[well].max() <= 1e-5, rel[well].max()
+        if (~well).any():
+            kmax = kappa.max(axis=1)[~well]
+            print(f"ell={ell}: other patterns: max rel / (8 kappa_max u) = {(rel[~well] / (8 * kmax * U)).max():.2e}")
     se_ref = ((ghat - G_ref.sum(axis=0)) ** 2).sum(axis=1)
     assert np.allclose(sqerr, se_ref, rtol=1e-4, atol=1e-10 * float((G_ref.sum(axis=0) ** 2).sum()))

@@ -1,9 +1,13 @@
 """GPU parity for regular-graph assignments (Algorithm 2) and the Sec. 4 simulation kernels.
 
 The assignment support is a random 8-regular graph on 200 vertices (the kind of
-expander the paper's approximate-GC experiments use); the oracle orders it with
-its own Algorithm 2 and the library receives that ordering through
-GC_ASSIGN_ORDER, so both sides see the same tables.
+expander the paper's approximate-GC experiments use).  The library orders it
+with its own Algorithm 2 (GC_ASSIGN_REGULAR).  Orderings are not unique (any
+perfect matching is a valid step), so the library's ordering is checked for
+what is fixed -- the support, one position 1..delta per chunk of each worker,
+every row sum delta(delta+1)/2 and the oracle's optimal Q_max -- and the
+kernels then run on it.  The decode/encode/combine parity also runs on the
+oracle's own ordering, handed over through GC_ASSIGN_ORDER.
 """
 from __future__ import annotations
 
@@ -36,18 +40,51 @@ def host(t):
     return t.cpu().numpy()
 
 
+def check_ordering(A, O):
+    """O is an ordering of the delta-regular support A that Algorithm 2 could return: same
+    support, each worker's chunks at positions 1..delta once each, every row summing to
+    delta(delta+1)/2, and the same (optimal) Q_max as the oracle's Algorithm 2."""
+    S = np.asarray(A) != 0
+    delta = int(S.sum(axis=0)[0])
+    assert np.array_equal(O != 0, S)
+    for j in range(S.shape[1]):
+        assert sorted(O[:, j][S[:, j]].tolist()) == list(range(1, delta + 1)), j
+    assert (O.sum(axis=1) == delta * (delta + 1) // 2).all()
+    assert OO.q_max(O) == OO.q_max(OO.chunk_ordering(A))
+    Q, qmax = gcx.gc_qmax(O)
+    assert np.array_equal(Q, OA.Q(O)) and qmax == OO.q_max(O)
+
+
 @functools.lru_cache(maxsize=None)
-def graph_tables(m=GRAPH.m, nu=GRAPH.delta):
+def graph_tables(source="regular", m=GRAPH.m, nu=GRAPH.delta):
     A = gen.random_regular_graph(m, nu)
-    O = OO.chunk_ordering(A)
-    _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, m, m, -1, O.astype(np.int32), nu, nu)
+    if source == "regular":
+        O, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_REGULAR, m, m, -1, A.astype(np.int32), nu, nu)
+        O = O.astype(np.int64)
+        check_ordering(A, O)
+        assert np.array_equal(OA.tables(O)[0], order)
+    else:
+        O = OO.chunk_ordering(A)
+        _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, m, m, -1, O.astype(np.int32), nu, nu)
     return O, order, holder, hpos
 
 
+@pytest.mark.parametrize("m,nu", [(12, 3), (200, 8), (300, 8)])
+def test_algorithm2_ordering(m, nu):
+    """GC_ASSIGN_REGULAR (Algorithm 2, Hopcroft-Karp matchings) on random regular graphs,
+    including the sizes of the paper's two graphs, against the oracle's Algorithm 2."""
+    A = gen.random_regular_graph(m, nu)
+    O, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_REGULAR, m, m, -1, A.astype(np.int32), nu, nu)
+    check_ordering(A, O.astype(np.int64))
+    o_ref, h_ref, p_ref = OA.tables(O.astype(np.int64))
+    assert np.array_equal(order, o_ref) and np.array_equal(holder, h_ref) and np.array_equal(hpos, p_ref)
+
+
+@pytest.mark.parametrize("source", ["regular", "oracle"])
 @pytest.mark.parametrize("ell", [1, 2, 3])
-def test_graph_assignment_decode_encode_combine(ell):
+def test_graph_assignment_decode_encode_combine(ell, source):
     wl = GRAPH
-    O, order, holder, hpos = graph_tables()
+    O, order, holder, hpos = graph_tables(source)
     psi = gen.psi(wl, count=300)
     R = gen.shared_R(wl.m, ell)
     cov, dec, cerr, Bc = gcx.gc_decode_coeffs(dev(psi), dev(order), dev(holder), dev(hpos), dev(R))
