@@ -51,6 +51,7 @@ extern "C" {
 #define GC_EINVAL (-1)  /* bad size, null pointer, bad enum, inconsistent tables  */
 #define GC_ELAUNCH (-2) /* the HIP runtime reported an error at launch           */
 #define GC_ENOTSUP (-3) /* the current device is not gfx950                      */
+#define GC_ESCRATCH (-4) /* the request needs more than the fixed scratch array   */
 
 /* assignment kinds for gc_assign */
 #define GC_ASSIGN_CYCLIC 0 /* cyclic scheme, N = m, worker j holds j..j+s (mod N) */
@@ -220,6 +221,25 @@ size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t el
 int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
                    int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * gc_reconstruct_noalloc -- gc_reconstruct for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and the same results, with the squared error's
+ * per-piece partial sums in a fixed array the library holds on each device
+ * (GC_NOALLOC_SCRATCH_BYTES, kept until the process ends) instead of a caller
+ * workspace.  Arguments and outputs as in gc_reconstruct; the caller still owns
+ * T, R, psi, ghat, gsum and sqerr.  Returns GC_ESCRATCH, with nothing enqueued,
+ * when gc_reconstruct_workspace_size(P, m, d, ell) exceeds
+ * GC_NOALLOC_SCRATCH_BYTES (split the patterns into smaller calls).  Calls no
+ * allocating routine.  All calls on one device share that device's array:
+ * calls that may overlap on one device (different streams, different host
+ * threads) race and must be serialised by the caller.
+ */
+#define GC_NOALLOC_SCRATCH_BYTES (4u << 20)
+int gc_reconstruct_noalloc(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m,
+                           int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
+                           hipStream_t stream);
 
 /*
  * gc_decode_direct -- the same estimate as gc_decode_coeffs + gc_encode +

@@ -19,6 +19,7 @@ extern "C" const char *gc_strerror(int status) {
     case GC_EINVAL: return "invalid argument";
     case GC_ELAUNCH: return "HIP launch or runtime error";
     case GC_ENOTSUP: return "device is not gfx950";
+    case GC_ESCRATCH: return "request exceeds the fixed scratch array of the no-allocation call";
     default: return "unknown status";
   }
 }

@@ -24,6 +24,8 @@
 // traffic (~0.6 ms at the 16384 x 10,000-pattern size with one 16 KB write per item);
 // written in 128 KB bursts, 8 / ell items' worth held in LDS per block, they cost
 // about a third less.
+#include <mutex>
+
 #include "common.h"
 
 namespace gcx {
@@ -315,50 +317,131 @@ extern "C" size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d,
   return pieces > 1 ? sizeof(double) * size_t(P) * size_t(pieces) : 0;
 }
 
-extern "C" int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P,
-                              int32_t m, int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
-                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
-  using namespace gcx;
-  if (P < 0 || m < 1 || m > GC_MAX_M || d < 1 || ell < 1 || ell > GC_MAX_ELL) return GC_EINVAL;
-  if (P == 0) return GC_OK;
-  if (!T || !R || !psi) return GC_EINVAL;
-  const bool want_err = sqerr != nullptr;
-  if (want_err && !gsum) return GC_EINVAL;
-  if (!ghat && !want_err) return GC_OK;  // nothing requested
+namespace gcx {
+namespace {
+
+// The combine behind both entry points: `partial` holds the squared error's per-piece sums
+// (P * pieces doubles) when there is more than one piece per pattern.
+int reconstruct_impl(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m, int64_t d,
+                     int32_t ell, float *ghat, const float *gsum, double *sqerr, double *partial,
+                     hipStream_t stream) {
   const int64_t L = ceil_div(d, ell);
   const int64_t pieces = rec_pieces(L);
-  if (!grid_ok(P * pieces, kRecThreads)) return GC_EINVAL;
-  double *partial = nullptr;
-  if (want_err) {
-    if (pieces == 1) {
-      partial = sqerr;
-    } else {
-      const size_t need = gc_reconstruct_workspace_size(P, m, d, ell);
-      if (!workspace || workspace_bytes < need) return GC_EINVAL;
-      partial = static_cast<double *>(workspace);
-    }
-  }
-  const int dev = check_device();
-  if (dev != GC_OK) return dev;
+  if (sqerr && pieces == 1) partial = sqerr;
   // float4 path: rows of T, the estimate's rows and gsum all 16-byte aligned
   const bool vec4 = L % 4 == 0 && d % 4 == 0 && aligned16(T) && (!ghat || aligned16(ghat)) &&
                     (!gsum || aligned16(gsum));
   (void)hipGetLastError();
   int st = GC_OK;
   switch (ell) {
-#define GC_CASE(E)                                                                           \
-  case E:                                                                                    \
-    st = launch_rec<E>(vec4, T, R, psi, P, m, d, L, pieces, ghat, gsum, partial, stream);    \
+#define GC_CASE(E)                                                                                 \
+  case E:                                                                                          \
+    st = launch_rec<E>(vec4, T, R, psi, P, m, d, L, pieces, ghat, sqerr ? gsum : nullptr,          \
+                       sqerr ? partial : nullptr, stream);                                         \
     break;
     GC_CASE(1) GC_CASE(2) GC_CASE(3) GC_CASE(4) GC_CASE(5) GC_CASE(6) GC_CASE(7) GC_CASE(8)
 #undef GC_CASE
     default: return GC_EINVAL;
   }
   if (st != GC_OK) return st;
-  if (want_err && pieces > 1)
-    hipLaunchKernelGGL(sqerr_finalize_kernel, dim3(unsigned(ceil_div(P, 256))), dim3(256), 0,
-                       stream, partial, P, int(pieces), sqerr);
+  if (sqerr && pieces > 1)
+    hipLaunchKernelGGL(sqerr_finalize_kernel, dim3(unsigned(ceil_div(P, 256))), dim3(256), 0, stream,
+                       partial, P, int(pieces), sqerr);
   return launch_status();
+}
+
+// Argument checks shared by both entry points (sizes, pointers, grid limits).  Returns
+// GC_OK to go on, or the status to return; *done = true when there is nothing to do.
+int reconstruct_check(const float *T, const float *R, const int32_t *psi, int64_t P, int32_t m, int64_t d,
+                      int32_t ell, const float *ghat, const float *gsum, const double *sqerr, bool *done) {
+  *done = false;
+  if (P < 0 || m < 1 || m > GC_MAX_M || d < 1 || ell < 1 || ell > GC_MAX_ELL) return GC_EINVAL;
+  if (P == 0) {
+    *done = true;
+    return GC_OK;
+  }
+  if (!T || !R || !psi) return GC_EINVAL;
+  if (sqerr && !gsum) return GC_EINVAL;
+  if (!ghat && !sqerr) {  // nothing requested
+    *done = true;
+    return GC_OK;
+  }
+  if (!grid_ok(P * rec_pieces(ceil_div(d, ell)), kRecThreads)) return GC_EINVAL;
+  return GC_OK;
+}
+
+}  // namespace
+}  // namespace gcx
+
+extern "C" int gc_reconstruct(const float *T, const float *R, const int32_t *psi, int64_t P,
+                              int32_t m, int64_t d, int32_t ell, float *ghat, const float *gsum, double *sqerr,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  using namespace gcx;
+  bool done = false;
+  const int chk = reconstruct_check(T, R, psi, P, m, d, ell, ghat, gsum, sqerr, &done);
+  if (chk != GC_OK || done) return chk;
+  const size_t need = sqerr ? gc_reconstruct_workspace_size(P, m, d, ell) : 0;
+  if (need && (!workspace || workspace_bytes < need)) return GC_EINVAL;
+  const int dev = check_device();
+  if (dev != GC_OK) return dev;
+  return reconstruct_impl(T, R, psi, P, m, d, ell, ghat, gsum, sqerr, static_cast<double *>(workspace),
+                          stream);
+}
+
+// ---------------------------------------------------------------------------------------
+// gc_reconstruct_noalloc: the same combine with its scratch (the squared error's per-piece
+// sums) in a fixed device array, for callers that cannot allocate.  Each device holds its
+// own copy of `scratch`; its address is looked up once per device with the device current
+// (the array's name in host code is only a stand-in for the symbol, not a device address).
+// Every call on a device shares that device's array: calls that overlap on one device race.
+// Nothing needs clearing: every partial sum a call reads, the same call has written.
+
+static __device__ __align__(256) double scratch[GC_NOALLOC_SCRATCH_BYTES / sizeof(double)];
+
+namespace gcx {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices];
+
+int scratch_address(void **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return GC_ELAUNCH;
+  if (dev < 0 || dev >= kMaxDevices) return GC_ENOTSUP;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return GC_ELAUNCH;
+    }
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return GC_OK;
+}
+
+}  // namespace
+}  // namespace gcx
+
+extern "C" int gc_reconstruct_noalloc(const float *T, const float *R, const int32_t *psi, int64_t P,
+                                      int32_t m, int64_t d, int32_t ell, float *ghat, const float *gsum,
+                                      double *sqerr, hipStream_t stream) {
+  using namespace gcx;
+  bool done = false;
+  const int chk = reconstruct_check(T, R, psi, P, m, d, ell, ghat, gsum, sqerr, &done);
+  if (chk != GC_OK || done) return chk;
+  const size_t need = sqerr ? gc_reconstruct_workspace_size(P, m, d, ell) : 0;
+  if (need > GC_NOALLOC_SCRATCH_BYTES) return GC_ESCRATCH;
+  const int dev = check_device();
+  if (dev != GC_OK) return dev;
+  void *ws = nullptr;
+  if (need) {
+    const int st = scratch_address(&ws);
+    if (st != GC_OK) return st;
+  }
+  return reconstruct_impl(T, R, psi, P, m, d, ell, ghat, gsum, sqerr, static_cast<double *>(ws), stream);
 }
 
 extern "C" int gc_sum_chunks(const void *G, int32_t g_dtype, int32_t N, int64_t d, float *gsum,

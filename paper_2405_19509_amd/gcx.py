@@ -15,7 +15,8 @@ from typing import Optional
 
 import numpy as np
 
-GC_OK, GC_EINVAL, GC_ELAUNCH, GC_ENOTSUP = 0, -1, -2, -3
+GC_OK, GC_EINVAL, GC_ELAUNCH, GC_ENOTSUP, GC_ESCRATCH = 0, -1, -2, -3, -4
+GC_NOALLOC_SCRATCH_BYTES = 4 << 20
 GC_ASSIGN_CYCLIC, GC_ASSIGN_ORDER, GC_ASSIGN_REGULAR = 0, 1, 2
 GC_LOSS_LINEAR, GC_LOSS_LOGISTIC = 0, 1
 GC_F32, GC_BF16 = 0, 1
@@ -46,6 +47,7 @@ SIGNATURES = {
     "gc_original_ls": (_c.c_int, [_p, _i64, _i32, _i32, _p, _i32, _p, _i32, _i32, _c.c_double, _p, _p, _p]),
     "gc_reconstruct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_reconstruct": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p, _sz, _p]),
+    "gc_reconstruct_noalloc": (_c.c_int, [_p, _p, _p, _i64, _i32, _i64, _i32, _p, _p, _p, _p]),
     "gc_decode_direct_workspace_size": (_sz, [_i64, _i32, _i64, _i32]),
     "gc_decode_direct": (_c.c_int, [_p, _i32, _i32, _i64, _p, _i64, _i32, _i32, _p, _p, _i32, _p,
                                     _i32, _p, _p, _p, _p, _sz, _p]),
@@ -291,6 +293,25 @@ def gc_reconstruct(T, R, d: int, psi, ghat=None, gsum=None, sqerr=None, want_gha
         _dev(sqerr, "sqerr", torch.float64, (P,)) if sqerr is not None else None,
         ws_ptr, ws_bytes, _stream(stream))
     _check("gc_reconstruct", st)
+    return ghat, sqerr
+
+
+def gc_reconstruct_noalloc(T, R, d: int, psi, ghat, gsum=None, sqerr=None, stream=None):
+    """gc_reconstruct without a workspace: the library's fixed per-device scratch array holds
+    the squared error's partial sums.  Outputs must be passed in (ghat [P][d] or None; sqerr
+    [P] fp64 with gsum [d], or None); nothing is allocated here.  Returns (ghat, sqerr)."""
+    torch = _torch()
+    P, m, L = T.shape
+    ell = R.shape[0]
+    if L != -(-d // ell):
+        raise ValueError("T's row length does not match ceil(d / ell)")
+    st = load().gc_reconstruct_noalloc(
+        _dev(T, "T", torch.float32), _dev(R, "R", torch.float32, (ell, m)),
+        _dev(psi, "psi", torch.int32, (P, m)), P, m, d, ell,
+        _dev(ghat, "ghat", torch.float32, (P, d)) if ghat is not None else None,
+        _dev(gsum, "gsum", torch.float32, (d,)) if gsum is not None else None,
+        _dev(sqerr, "sqerr", torch.float64, (P,)) if sqerr is not None else None, _stream(stream))
+    _check("gc_reconstruct_noalloc", st)
     return ghat, sqerr
 
 
