@@ -68,3 +68,22 @@ def test_traffic_follows_the_kernel_sources(tmp_path, monkeypatch):
     with open(csrc / "common.h", "a") as f:
         f.write("\n// edited\n")
     assert bench.measured_traffic(HEADLINE, "gc_reconstruct") is None
+
+
+def test_cpu_baseline_pool_runs_the_oracle():
+    """The oracle baseline's process pool: every pattern of the tiny workload on two worker
+    processes and a one-core sample; per-step CPU seconds, rates, the d-slice scaling."""
+    from workloads import BANDWIDTH, TINY
+    r = bench.cpu_oracle_config(TINY, 1, 2, one_core_count=10)
+    assert r["patterns"] == TINY.P and r["procs"] == 2
+    assert r["patterns_per_s"] > 0 and r["one_core"]["patterns"] == 10
+    assert set(r["cpu_seconds"]) == {"chunk_grads", "decode_coeffs", "encode", "reconstruct"}
+    s = bench.cpu_oracle_config(BANDWIDTH, 1, 2, count=2, cols=slice(0, 64))
+    assert s["d_slice"].startswith("64 of 1048576") and s["patterns_per_s"] > 0
+
+
+def test_pattern_windows_cover_every_pattern_once():
+    for P, parts in ((10000, 64), (100000, 160), (7, 3), (1, 5)):
+        w = bench._windows(P, parts)
+        assert w[0][0] == 0 and w[-1][1] == P
+        assert all(a[1] == b[0] for a, b in zip(w, w[1:])) and all(lo < hi for lo, hi in w)
