@@ -254,8 +254,16 @@ namespace {
 bool fused_ok(int64_t d) { return d % 4 == 0 && d <= int64_t(gcx::kFusedThreads) * 4 * gcx::kFusedMaxNV; }
 }  // namespace
 
+namespace {
+// X [N][n][d], W [b][d], G [b][N][d], residuals [b][N][n]
+bool grad_sizes_ok(int32_t N, int32_t n, int64_t d, int32_t b) {
+  return N >= 1 && n >= 1 && d >= 1 && b >= 1 && gcx::sizes_ok({N, n, d}) && gcx::sizes_ok({b, N, d}) &&
+         gcx::sizes_ok({b, N, n});
+}
+}  // namespace
+
 extern "C" size_t gc_chunk_grads_workspace_size(int32_t N, int32_t n, int64_t d, int32_t b) {
-  if (N < 1 || n < 1 || d < 1 || b < 1) return 0;
+  if (!grad_sizes_ok(N, n, d, b)) return 0;
   if (gcx::mfma_eligible(d, b)) return gcx::mfma_workspace_bytes(N, n, d, b);
   if (fused_ok(d)) {
     const gcx::FusedPlan fp = gcx::fused_plan(N, n);
@@ -268,7 +276,7 @@ extern "C" int gc_chunk_grads(const float *X, const float *y, const float *W, in
                               int64_t d, int32_t b, int32_t loss, float *G, void *workspace,
                               size_t workspace_bytes, hipStream_t stream) {
   using namespace gcx;
-  if (N < 1 || n < 1 || d < 1 || b < 1) return GC_EINVAL;
+  if (!grad_sizes_ok(N, n, d, b)) return GC_EINVAL;
   if (loss != GC_LOSS_LINEAR && loss != GC_LOSS_LOGISTIC) return GC_EINVAL;
   if (!X || !y || !W || !G || !workspace) return GC_EINVAL;
   if (workspace_bytes < gc_chunk_grads_workspace_size(N, n, d, b)) return GC_EINVAL;

@@ -5,6 +5,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <initializer_list>
 
 #include "gcx.h"
 
@@ -45,7 +46,30 @@ inline int launch_status() {
 
 inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+// ceil(a / b) for a >= 0, b > 0, without forming a + b - 1 (no overflow near INT64_MAX)
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return a / b + (a % b != 0 ? 1 : 0); }
+
+// Host-side size limits: no array extent above 2^40 and no array above 2^48 elements
+// (neither fits on any device), so that every size the entry points derive from their
+// arguments is formed without int64 overflow.
+constexpr int64_t kMaxExtent = int64_t(1) << 40;
+constexpr int64_t kMaxElems = int64_t(1) << 48;
+
+// every extent in [0, kMaxExtent] and their product at most kMaxElems
+inline bool sizes_ok(std::initializer_list<int64_t> dims) {
+  bool zero = false;
+  for (int64_t v : dims) {
+    if (v < 0 || v > kMaxExtent) return false;
+    zero = zero || v == 0;
+  }
+  if (zero) return true;
+  int64_t prod = 1;
+  for (int64_t v : dims) {
+    if (prod > kMaxElems / v) return false;
+    prod *= v;
+  }
+  return true;
+}
 
 // A 1-D launch must keep gridDim.x < 2^31 and the total thread count < 2^32.
 inline bool grid_ok(int64_t blocks, int threads) {

@@ -636,6 +636,8 @@ extern "C" int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_
   if (P < 0 || N < 1 || m < 1 || m > GC_MAX_M || delta < 1 || delta > GC_MAX_DELTA ||
       gamma < 1 || gamma > GC_MAX_DELTA || ell < 1 || ell > GC_MAX_ELL)
     return GC_EINVAL;
+  // psi [P][m], cov [P][N], Bc [P][m][delta][ell]
+  if (!sizes_ok({P, m, delta, ell}) || !sizes_ok({P, N}) || !sizes_ok({N, gamma})) return GC_EINVAL;
   if (P == 0) return GC_OK;
   if (!grid_ok(ceil_div(P, kDecodeWaves), kDecodeThreads)) return GC_EINVAL;
   if (!psi || !order || !holder || !hpos || !dec || !coef_err) return GC_EINVAL;

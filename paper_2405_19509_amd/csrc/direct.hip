@@ -469,7 +469,9 @@ size_t direct_c_bytes(int64_t P, int N, int ell) {
 
 extern "C" size_t gc_decode_direct_workspace_size(int64_t P, int32_t N, int64_t d, int32_t ell) {
   using namespace gcx;
-  if (P < 1 || N < 1 || d < 1 || ell < 1 || ell > GC_MAX_ELL) return 0;
+  if (P < 1 || N < 1 || d < 1 || ell < 1 || ell > GC_MAX_ELL || !sizes_ok({P, ell, direct_kp(N, ell)}) ||
+      !sizes_ok({P, d}))
+    return 0;
   const int64_t ntiles = ceil_div(ceil_div(d, ell), kDN);
   return direct_c_bytes(P, N, ell) + sizeof(double) * size_t(P) * ell * size_t(ntiles);
 }
@@ -485,6 +487,9 @@ extern "C" int gc_decode_direct(const void *G, int32_t g_dtype, int32_t N, int64
       delta > GC_MAX_DELTA ||
       gamma < 1 || gamma > GC_MAX_DELTA || ell < 1 || ell > GC_MAX_ELL ||
       (g_dtype != GC_F32 && g_dtype != GC_BF16))
+    return GC_EINVAL;
+  // G [N][d], psi [P][m], the estimate [P][d], mixing rows [P ell][Kp]
+  if (!sizes_ok({N, d}) || !sizes_ok({P, m}) || !sizes_ok({P, d}) || !sizes_ok({P, ell, direct_kp(N, ell)}))
     return GC_EINVAL;
   if (P == 0) return GC_OK;
   if (!G || !psi || !holder || !hpos || !R || !workspace) return GC_EINVAL;

@@ -963,6 +963,9 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
   if (N < 1 || d < 1 || P < 0 || m < 1 || m > GC_MAX_M || delta < 1 || delta > GC_MAX_DELTA ||
       ell < 1 || ell > GC_MAX_ELL || (g_dtype != GC_F32 && g_dtype != GC_BF16))
     return GC_EINVAL;
+  // G [N][d], Bc [P][m][delta][ell], T [P][m][L]
+  if (!sizes_ok({N, d}) || !sizes_ok({P, m, delta, ell}) || !sizes_ok({P, m, ceil_div(d, ell)}))
+    return GC_EINVAL;
   if (P == 0) return GC_OK;
   if (!G || !psi || !order || !Bc || !T) return GC_EINVAL;
   const int dev = check_device();

@@ -311,8 +311,9 @@ __global__ void sum_chunks_kernel(const void *__restrict__ G, int bf16, int N, i
 }  // namespace gcx
 
 extern "C" size_t gc_reconstruct_workspace_size(int64_t P, int32_t m, int64_t d, int32_t ell) {
-  (void)m;
-  if (P < 1 || d < 1 || ell < 1 || ell > GC_MAX_ELL) return 0;
+  if (P < 1 || m < 1 || d < 1 || ell < 1 || ell > GC_MAX_ELL || !gcx::sizes_ok({P, d}) ||
+      !gcx::sizes_ok({P, m, gcx::ceil_div(d, ell)}))
+    return 0;
   const int64_t pieces = gcx::rec_pieces(gcx::ceil_div(d, ell));
   return pieces > 1 ? sizeof(double) * size_t(P) * size_t(pieces) : 0;
 }
@@ -356,6 +357,8 @@ int reconstruct_check(const float *T, const float *R, const int32_t *psi, int64_
                       int32_t ell, const float *ghat, const float *gsum, const double *sqerr, bool *done) {
   *done = false;
   if (P < 0 || m < 1 || m > GC_MAX_M || d < 1 || ell < 1 || ell > GC_MAX_ELL) return GC_EINVAL;
+  // T [P][m][L], the estimate [P][d]
+  if (!sizes_ok({P, d}) || !sizes_ok({P, m, ceil_div(d, ell)})) return GC_EINVAL;
   if (P == 0) {
     *done = true;
     return GC_OK;
@@ -448,6 +451,7 @@ extern "C" int gc_sum_chunks(const void *G, int32_t g_dtype, int32_t N, int64_t 
                              hipStream_t stream) {
   using namespace gcx;
   if (N < 1 || d < 1 || !G || !gsum || (g_dtype != GC_F32 && g_dtype != GC_BF16)) return GC_EINVAL;
+  if (!sizes_ok({N, d})) return GC_EINVAL;
   if (!grid_ok(ceil_div(d, 256), 256)) return GC_EINVAL;
   const int dev = check_device();
   if (dev != GC_OK) return dev;

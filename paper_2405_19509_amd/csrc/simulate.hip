@@ -227,6 +227,8 @@ extern "C" int gc_progress(const double *tau, const uint8_t *failed, int64_t R, 
                            hipStream_t stream) {
   using namespace gcx;
   if (R < 0 || m < 1 || m > GC_MAX_M || delta < 1 || delta > GC_MAX_DELTA || G < 1) return GC_EINVAL;
+  // tau [R][m][delta], psi [R][G][m]
+  if (!sizes_ok({R, m, delta}) || !sizes_ok({R, G, m})) return GC_EINVAL;
   if (R == 0) return GC_OK;
   if (!tau || !T || !psi) return GC_EINVAL;
   const int64_t blocks = ceil_div(R * m, kSimThreads);
@@ -247,6 +249,7 @@ extern "C" int gc_completion_times(const double *tau, const uint8_t *failed, int
   if (R < 0 || N < 1 || m < 1 || m > GC_MAX_M || delta < 1 || delta > GC_MAX_DELTA || gamma < 1 ||
       gamma > GC_MAX_DELTA || ell < 1 || ell > GC_MAX_ELL)
     return GC_EINVAL;
+  if (!sizes_ok({R, m, delta}) || !sizes_ok({N, gamma})) return GC_EINVAL;  // tau, tables
   if (R == 0) return GC_OK;
   if (!tau || !holder || !hpos || !partial || !original) return GC_EINVAL;
   const int64_t blocks = ceil_div(R, kSimWaves);
@@ -267,6 +270,7 @@ extern "C" int gc_original_ls(const int32_t *psi, int64_t P, int32_t N, int32_t 
   if (P < 0 || N < 1 || N > GC_MAX_M || m < 1 || m > GC_MAX_M || delta < 1 ||
       delta > GC_MAX_DELTA || gamma < 1 || gamma > GC_MAX_DELTA || max_iter < 0 || !(tol >= 0.0))
     return GC_EINVAL;
+  if (!sizes_ok({P, m})) return GC_EINVAL;  // psi [P][m]
   if (P == 0) return GC_OK;
   if (!psi || !order || !holder || !err) return GC_EINVAL;
   if (!grid_ok(P, kLsThreads)) return GC_EINVAL;
