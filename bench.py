@@ -544,10 +544,12 @@ def device_G(wl, dev, seed=0):
 
 def large_batch(ell, override):
     """Patterns per encode/combine call on the m = 200 workload (T is 13.4 GB per pattern at
-    ell = 1): as many as keep T near 110 GB, so G's 6.7 GB are read once per several patterns."""
+    ell = 1): as many as keep T near 215 GB, so G's 6.7 GB are read once per 16 / 32 / 64
+    patterns and the matrix-core encode gets 16 / 32 patterns per tile (measured: 16 patterns
+    per call write T 20% faster than 8 at ell = 1)."""
     if override:
         return override
-    return {1: 8, 2: 16, 4: 32}.get(ell, 8)
+    return {1: 16, 2: 32, 4: 64}.get(ell, 16)
 
 
 def run_configs(gcx, args, dev, psi_large):

@@ -25,6 +25,7 @@
 // When the slice of every chunk does not fit in LDS (many chunks, ell >= 2, bf16 at
 // large N) the worker-group layout below takes over.
 #include "common.h"
+#include "encode_mx.h"
 
 namespace gcx {
 namespace {
@@ -992,6 +993,11 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
   const int vec = (a.L % 4 == 0 && (ta & 15) == 0) ? 4 : ((a.L % 2 == 0 && (ta & 7) == 0) ? 2 : 1);
   const bool all_chunks = size_t(N) * ell * kWave * vec * esize <= kEncSliceLds;
   (void)hipGetLastError();
+  // bf16 chunk gradients beyond the all-chunk layout: the bf16 matrix cores, where they fit
+  if (g_dtype == GC_BF16 && !all_chunks) {
+    const int st = encode_mx(G, N, d, psi, order, Bc, P, m, delta, ell, T, stream);
+    if (st != kEncodeMxNotApplicable) return st != GC_OK ? st : launch_status();
+  }
   const int st = g_dtype == GC_F32 ? dispatch_encode<float>(a, P, vec, all_chunks, stream)
                                    : dispatch_encode<uint16_t>(a, P, vec, all_chunks, stream);
   if (st != GC_OK) return st;

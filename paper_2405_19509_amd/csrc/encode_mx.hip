@@ -1,0 +1,356 @@
+// gc_encode on the bf16 matrix cores, for bf16 chunk gradients (Sec. 2, worker encode):
+//   T[p][j][x] = sum_{t < psi[p][j]} sum_{k < ell} Bc[p][j][t][k] * g_{order[j][t]}[k*L + x]
+//
+// Why matrix cores: every output value of the encode takes psi*ell multiply-adds, 4-5 per
+// byte of T at delta = 20, ell = 1 and 4x that at ell = 4, which the vector units cannot
+// sustain at the HBM write rate.  Per worker group the encode is a dense contraction
+//   T[(pattern, worker)][x] = sum_kk A[(pattern, worker)][kk] * Gs[kk][x]
+// over kk = (chunk slot s of the group's union, block k), with A the coefficients of the
+// row's worker (zero where the worker does not hold the chunk or has not processed it).
+//
+// Arithmetic: the chunk gradients are bf16 already; each fp32 coefficient a is split
+// exactly into three bf16 parts a = a1 + a2 + a3 + r with |r| <= 2^-24 |a| (each part is
+// the bf16 rounding of what the previous ones leave), and the three products per term
+// (exact in fp32: 8 x 8 significant bits) are accumulated in fp32 by
+// v_mfma_f32_32x32x16_bf16.  Error per output: at most u sum |a||g| from the split plus
+// the fp32 accumulation of 3 psi ell products, against psi ell for the vector path.
+//
+// Layout: a block owns a group of J consecutive workers, a tile of PB patterns
+// (J * PB = 32 rows (pattern, worker), row r = pb * J + jb) and a range of 512-wide
+// slices of x walked in turn.  Per slice it stages, straight from memory to LDS, the
+// slices of the group's union of chunks (J + delta - 1 chunks under the cyclic order),
+// one 1 KB row per (slot, block); the coefficient tile, split into its three bf16
+// planes, is built once per block.  Each of the 8 waves computes two 32 x 32 output
+// tiles per slice: per 16-deep K step three bf16x8 coefficient loads, eight 16-bit
+// gathers of the staged column per tile, six MFMAs.  Stores are 4 bytes per lane, two
+// 128-byte row segments per instruction, non-temporal; rows of workers that transmit
+// nothing (psi = 0) are not written.  Blocks of a slice range run back to back on one
+// XCD (round-robin dispatch), so its L2 serves the groups' overlapping chunk slices.
+// If a block's union exceeds its slots (orders other than the cyclic one), it walks its
+// workers one at a time (a pass per worker, each staging only that worker's chunks).
+#include "common.h"
+#include "encode_mx.h"
+
+namespace gcx {
+namespace {
+
+constexpr int kMxThreads = 512;
+constexpr int kMxWaves = kMxThreads / kWave;
+constexpr int kMxW = 512;                    // positions per slice (1 KB of bf16 per staged row)
+constexpr int kMxRowBytes = kMxW * 2 + 16;   // staged row stride: padded so rows 8 apart differ in bank
+constexpr int kMxMaxKS = 6;                  // K steps of 16 (at most 96 staged rows)
+constexpr size_t kMxLds = 152 * 1024;
+
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// round-to-nearest-even bf16 bits of a finite fp32 value
+__device__ __forceinline__ uint32_t bf16_rne(float v) {
+  const uint32_t b = __float_as_uint(v);
+  return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
+}
+
+struct MxArgs {
+  const uint16_t *G;
+  int N;
+  int64_t d, L;
+  const int32_t *psi;
+  const int32_t *order;
+  const float *Bc;
+  int64_t P;
+  int m, delta, ell;
+  float *T;
+  bool stage16;   // G rows 16-byte aligned and d, L multiples of 8
+  int J;          // workers per tile
+  int PB;         // patterns per tile
+  int ngroups;
+  int64_t ntp;    // pattern tiles
+  int slots;      // union slots staged per block
+  int nslices;
+  int64_t spb;    // slices per range
+  int64_t nsr;    // slice ranges (a multiple of 8)
+};
+
+// LDS: [ Gs: Kp rows x kMxRowBytes ][ Ap: 3 planes x 32 rows x AP bf16 ][ rdesc: 2 int64 per row ]
+//      [ map: N int32 ][ slotc: slots int32 ][ code: J*delta int32 ]
+// The coefficient tile is first assembled in fp32 over the Gs region, then split into Ap.
+template <int KS>
+__global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4))) void encode_mx_kernel(MxArgs a) {
+  constexpr int Kp = 16 * KS;
+  constexpr int AP = Kp + 8;  // plane row stride (bf16): 16-byte aligned rows, staggered banks
+  extern __shared__ __align__(16) unsigned char lds[];
+  unsigned char *Gs = lds;
+  uint16_t *Ap = reinterpret_cast<uint16_t *>(lds + size_t(Kp) * kMxRowBytes);
+  int64_t *rdesc = reinterpret_cast<int64_t *>(Ap + 3 * 32 * AP);
+  int32_t *map = reinterpret_cast<int32_t *>(rdesc + 2 * Kp);
+  int32_t *slotc = map + a.N;
+  int32_t *code = slotc + a.slots;
+  float *Af = reinterpret_cast<float *>(Gs);  // [32][Kp] fp32, before the slices are staged
+  __shared__ int nslot_s, nuni_s;
+  __shared__ uint32_t rsend_s;
+  __shared__ int64_t rowoff_s[32];  // element offset of each tile row (pattern, worker) in T
+
+  // block -> (slice range, unit = (group, pattern tile)); XCD x takes ranges x, x + 8, ...
+  const int64_t b = blockIdx.x;
+  const int64_t units = int64_t(a.ngroups) * a.ntp;
+  const int64_t sr = (b & 7) + 8 * ((b >> 3) / units);
+  const int64_t unit = (b >> 3) % units;
+  const int64_t s_begin = sr * a.spb;
+  const int64_t s_end = s_begin + a.spb < a.nslices ? s_begin + a.spb : a.nslices;
+  if (s_begin >= s_end) return;  // the whole block: an empty range at the end
+  const int gi = int(unit % a.ngroups);
+  const int64_t p0 = (unit / a.ngroups) * a.PB;
+  const int j0 = gi * a.J;
+  const int nj = a.m - j0 < a.J ? a.m - j0 : a.J;
+  const int ell = a.ell;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int lane = tid % kWave, h = lane >> 5, li = lane & 31;
+
+  // which chunks the whole group uses; if they exceed the slots, one worker per pass
+  for (int c = tid; c < a.N; c += kMxThreads) map[c] = 0;
+  __syncthreads();
+  for (int e = tid; e < nj * a.delta; e += kMxThreads) {
+    const int c = a.order[int64_t(j0) * a.delta + e];
+    if (c >= 0 && c < a.N) map[c] = 1;
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    int cnt = 0;
+    for (int base = 0; base < a.N; base += kWave) {
+      const int c = base + tid;
+      const unsigned long long mk = __ballot(c < a.N && map[c] != 0);
+      cnt += __popcll(mk);
+    }
+    if (tid == 0) nuni_s = cnt;
+  }
+  __syncthreads();
+  const bool split = nuni_s > a.slots;
+  const int npass = split ? nj : 1;
+
+  for (int pass = 0; pass < npass; ++pass) {
+    // active workers of this pass: all nj, or worker jb = pass
+    const int ja = split ? pass : 0, jn = split ? pass + 1 : nj;
+    __syncthreads();  // the previous pass is done with every table
+    for (int c = tid; c < a.N; c += kMxThreads) map[c] = 0;
+    __syncthreads();
+    for (int e = tid; e < (jn - ja) * a.delta; e += kMxThreads) {
+      const int c = a.order[int64_t(j0 + ja) * a.delta + e];
+      if (c >= 0 && c < a.N) map[c] = 1;
+    }
+    __syncthreads();
+    // slots in ascending chunk order
+    if (tid < kWave) {
+      int cnt = 0;
+      for (int base = 0; base < a.N; base += kWave) {
+        const int c = base + tid;
+        const bool on = c < a.N && map[c] != 0;
+        const unsigned long long mk = __ballot(on);
+        if (on) {
+          const int s = cnt + __popcll(mk & ((1ull << tid) - 1));
+          map[c] = s;  // < slots: the active set fits by construction
+          slotc[s] = c;
+        } else if (c < a.N) {
+          map[c] = -1;
+        }
+        cnt += __popcll(mk);
+      }
+      if (tid == 0) nslot_s = cnt;
+    }
+    __syncthreads();
+    const int nslot = nslot_s;
+    const int K = nslot * ell;
+    // per (worker, position): the slot of the chunk there, or -1
+    for (int e = tid; e < nj * a.delta; e += kMxThreads) {
+      const int jb = e / a.delta;
+      const int c = a.order[int64_t(j0 + jb) * a.delta + e % a.delta];
+      code[e] = (jb >= ja && jb < jn && c >= 0 && c < a.N) ? map[c] : -1;
+    }
+    for (int e = tid; e < 32 * Kp; e += kMxThreads) Af[e] = 0.f;
+    __syncthreads();
+    // the coefficient tile: row r = (pattern p0 + r / J, worker j0 + r % J), column
+    // s*ell + k; zero past each row's processed prefix
+    for (int e = tid; e < 32 * a.delta; e += kMxThreads) {
+      const int r = e / a.delta, t = e % a.delta;
+      const int pb = r / a.J, jb = r % a.J;
+      const int64_t p = p0 + pb;
+      if (pb >= a.PB || p >= a.P || jb >= nj) continue;
+      const int s = code[jb * a.delta + t];
+      if (s < 0) continue;
+      int v = a.psi[p * a.m + j0 + jb];
+      v = v < 0 ? 0 : (v > a.delta ? a.delta : v);
+      if (t >= v) continue;
+      const float *src = a.Bc + ((p * a.m + j0 + jb) * a.delta + t) * ell;
+      for (int k = 0; k < ell; ++k) Af[r * Kp + s * ell + k] = src[k];
+    }
+    if (tid < kWave) {
+      bool on = false;
+      if (tid < 32) {
+        const int pb = tid / a.J, jb = tid % a.J;
+        const int64_t p = p0 + pb;
+        if (pb < a.PB && p < a.P && jb >= ja && jb < jn) on = a.psi[p * a.m + j0 + jb] > 0;
+      }
+      const unsigned long long mk = __ballot(on);
+      if (tid == 0) rsend_s = uint32_t(mk);
+      if (tid < 32) rowoff_s[tid] = ((p0 + tid / a.J) * a.m + j0 + tid % a.J) * a.L;
+    }
+    __syncthreads();
+    // three bf16 planes: a1 = bf16(a), a2 = bf16(a - a1), a3 = bf16(a - a1 - a2), all exact steps
+    for (int e = tid; e < 32 * Kp; e += kMxThreads) {
+      const int r = e / Kp, kk = e % Kp;
+      const float v = Af[e];
+      const uint32_t b1 = bf16_rne(v);
+      const float r1 = v - __uint_as_float(b1 << 16);
+      const uint32_t b2 = bf16_rne(r1);
+      const float r2 = r1 - __uint_as_float(b2 << 16);
+      const uint32_t b3 = bf16_rne(r2);
+      Ap[(0 * 32 + r) * AP + kk] = uint16_t(b1);
+      Ap[(1 * 32 + r) * AP + kk] = uint16_t(b2);
+      Ap[(2 * 32 + r) * AP + kk] = uint16_t(b3);
+    }
+    // staged rows: element offset of block k of slot s's chunk, and the end of its valid
+    // positions min(L, d - k L)
+    for (int row = tid; row < K; row += kMxThreads) {
+      const int s = row / ell, k = row % ell;
+      rdesc[2 * row] = int64_t(slotc[s]) * a.d + int64_t(k) * a.L;
+      const int64_t rem = a.d - int64_t(k) * a.L;
+      rdesc[2 * row + 1] = rem < a.L ? rem : a.L;
+    }
+    __syncthreads();  // Af consumed: the slice region is free
+    // rows K .. Kp of the slice region stay zero for the whole pass
+    for (int e = tid; e < (Kp - K) * (kMxRowBytes / 16); e += kMxThreads)
+      reinterpret_cast<uint4 *>(Gs + size_t(K) * kMxRowBytes)[e] = make_uint4(0u, 0u, 0u, 0u);
+    const uint32_t rsend = rsend_s;
+
+    for (int64_t slice = s_begin; slice < s_end; ++slice) {
+      const int64_t x0 = slice * kMxW;
+      __syncthreads();  // the previous slice is consumed
+      // stage: staged row `row` <- 512 positions of its block from x0 (zero past L or d);
+      // one wave instruction per row, lane i filling bytes 16i..16i+15 of its 1 KB
+      for (int row = wave; row < K; row += kMxWaves) {
+        const int64_t base = rdesc[2 * row], lim = rdesc[2 * row + 1];
+        const int64_t x = x0 + 8 * lane;
+        unsigned char *dst = Gs + size_t(row) * kMxRowBytes;
+        if (a.stage16 && x0 + kMxW <= lim) {
+          __builtin_amdgcn_global_load_lds(a.G + base + x, dst, 16, 0, 0);
+        } else {
+          uint32_t w[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t lo = x + 2 * q < lim ? a.G[base + x + 2 * q] : 0u;
+            const uint32_t hi = x + 2 * q + 1 < lim ? a.G[base + x + 2 * q + 1] : 0u;
+            w[q] = lo | (hi << 16);
+          }
+          *reinterpret_cast<uint4 *>(dst + 16 * lane) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's direct-to-LDS loads have landed
+      __syncthreads();
+
+      // two 32 x 32 tiles per wave: positions x0 + 64 wave + 32 c + li
+      v16f acc0 = {}, acc1 = {};
+      const uint16_t *Gc = reinterpret_cast<const uint16_t *>(Gs) + 64 * wave + li;
+      constexpr int GR = kMxRowBytes / 2;  // staged row stride in bf16
+#pragma unroll 1
+      for (int q = 0; q < KS; ++q) {
+        const int kb = 16 * q + 8 * h;
+        const v8bf a1 = *reinterpret_cast<const v8bf *>(Ap + (0 * 32 + li) * AP + kb);
+        const v8bf a2 = *reinterpret_cast<const v8bf *>(Ap + (1 * 32 + li) * AP + kb);
+        const v8bf a3 = *reinterpret_cast<const v8bf *>(Ap + (2 * 32 + li) * AP + kb);
+        v8bf b0, b1;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          b0[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR]);
+          b1[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR + 32]);
+        }
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b1, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b1, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc1, 0, 0, 0);
+      }
+      // lane (h, li) holds D[8(v/4) + 4h + v%4][li] of each tile
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = 8 * (v >> 2) + 4 * h + (v & 3);
+        if (!((rsend >> r) & 1u)) continue;
+        float *row = a.T + rowoff_s[r];
+        const int64_t xa = x0 + 64 * wave + li, xb = xa + 32;
+        if (xa < a.L) __builtin_nontemporal_store(acc0[v], row + xa);
+        if (xb < a.L) __builtin_nontemporal_store(acc1[v], row + xb);
+      }
+    }
+  }
+}
+
+template <int KS>
+int launch_mx_ks(const MxArgs &m, size_t lds, hipStream_t st) {
+  const int64_t blocks = m.nsr * m.ngroups * m.ntp;
+  if (!grid_ok(blocks, kMxThreads)) return GC_EINVAL;
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_mx_kernel<KS>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
+    return GC_ELAUNCH;
+  hipLaunchKernelGGL((encode_mx_kernel<KS>), dim3(unsigned(blocks)), dim3(kMxThreads), lds, st, m);
+  return GC_OK;
+}
+
+}  // namespace
+
+int encode_mx(const void *G, int32_t N, int64_t d, const int32_t *psi, const int32_t *order, const float *Bc,
+              int64_t P, int32_t m, int32_t delta, int32_t ell, float *T, hipStream_t stream) {
+  MxArgs a{};
+  a.G = static_cast<const uint16_t *>(G);
+  a.N = N;
+  a.d = d;
+  a.L = ceil_div(d, ell);
+  a.psi = psi;
+  a.order = order;
+  a.Bc = Bc;
+  a.P = P;
+  a.m = m;
+  a.delta = delta;
+  a.ell = ell;
+  a.T = T;
+  a.stage16 = d % 8 == 0 && a.L % 8 == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0;
+  // 32 rows: PB patterns (a power of two covering the call, at most 32) x J workers
+  int pb = 1;
+  while (pb < 32 && pb < P) pb *= 2;
+  a.PB = pb;
+  a.J = 32 / pb;
+  if (a.J > m) a.J = m;
+  a.ngroups = int(ceil_div(m, a.J));
+  a.ntp = ceil_div(P, pb);
+  // slots for the cyclic union of a group; a block whose union is larger walks its workers
+  // one at a time, each needing delta slots
+  int64_t slots = int64_t(a.J) + delta - 1;
+  if (slots > N) slots = N;
+  if (slots < delta) slots = delta;
+  a.slots = int(slots);
+  const int64_t K = slots * ell;
+  const int KS = int(ceil_div(K, 16));
+  if (KS > kMxMaxKS) return kEncodeMxNotApplicable;
+  const int Kp = 16 * KS;
+  const size_t lds = size_t(Kp) * kMxRowBytes + sizeof(uint16_t) * 3 * 32 * (Kp + 8) +
+                     2 * sizeof(int64_t) * size_t(Kp) + sizeof(int32_t) * (size_t(N) + slots + size_t(a.J) * delta);
+  if (lds > kMxLds) return kEncodeMxNotApplicable;
+  a.nslices = int(ceil_div(a.L, kMxW));
+  // slice ranges: a multiple of 8 (one share per XCD), about 16 blocks per CU in all
+  const int64_t units = int64_t(a.ngroups) * a.ntp;
+  const int64_t want = 16 * int64_t(cu_count());
+  int64_t nsr = ceil_div(ceil_div(want, units), 8) * 8;
+  if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
+  a.spb = ceil_div(a.nslices, nsr);
+  a.nsr = ceil_div(ceil_div(a.nslices, a.spb), 8) * 8;
+  switch (KS) {
+    case 1: return launch_mx_ks<1>(a, lds, stream);
+    case 2: return launch_mx_ks<2>(a, lds, stream);
+    case 3: return launch_mx_ks<3>(a, lds, stream);
+    case 4: return launch_mx_ks<4>(a, lds, stream);
+    case 5: return launch_mx_ks<5>(a, lds, stream);
+    case 6: return launch_mx_ks<6>(a, lds, stream);
+    default: return kEncodeMxNotApplicable;
+  }
+}
+
+}  // namespace gcx

@@ -21,6 +21,26 @@ def gamma(n):
     return n * U / (1.0 - n * U)
 
 
+def encode_bound(nterm, M, g_dtype="f32"):
+    """Elementwise bound on the GPU encode's |T - T_ref| for rows with nterm = psi*ell terms
+    of magnitude sum M = sum_{t,k} |Bc||g|.  fp32 chunk gradients: gamma_n M (one fp32 FMA
+    per term).  bf16 chunk gradients may run on the bf16 matrix cores: each coefficient is
+    split exactly into three bf16 parts, leaving at most u|a| unrepresented, and the 3n
+    products are accumulated in fp32; each accumulation is allowed 2u (the matrix cores'
+    rounding of their internal sums is not assumed to be to nearest): u M + gamma'_{3n+1} M
+    with gamma'_k = 2ku / (1 - 2ku).  That also bounds the vector path."""
+    return encode_eps(nterm, g_dtype)[..., None] * M
+
+
+def encode_eps(nterm, g_dtype="f32"):
+    """The factor of encode_bound: gamma_n (fp32), u + gamma'_{3n+1} (bf16)."""
+    nterm = np.asarray(nterm, dtype=np.float64)
+    if g_dtype != "bf16":
+        return gamma(nterm)
+    k = 3 * nterm + 1
+    return U + 2 * k * U / (1.0 - 2 * k * U)
+
+
 def coverage_all(O, psi):
     """cov [P][N], dec [P] (for each ell given later), via the oracle per pattern."""
     return np.stack([OP.coverage(O, p) for p in psi]).astype(np.int64)

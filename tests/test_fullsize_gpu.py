@@ -65,9 +65,10 @@ def check_sampled(O, order, psi, R, G, dtype, T_d, ghat_d, pats, xs, ell):
         T = host(T_d[p][:, xs_t]).astype(np.float64)
         sent = psi[p] > 0
         # sum of |terms| of each T entry; its error: fp32 rounding of the coefficients and the
-        # delta*ell-term fp32 sum, plus the fp64 Gram/Cholesky solve (~kappa^2 2^-53)
+        # delta*ell-term fp32 sum (for bf16 gradients the matrix cores' split-coefficient sum),
+        # plus the fp64 Gram/Cholesky solve (~kappa^2 2^-53)
         Mag = OP.encode(np.abs(B), np.abs(Gsub), ell)
-        eps_T = 2 * R_.gamma(ell * delta + 2) + 1e-14 * kap ** 2
+        eps_T = max(2 * R_.gamma(ell * delta + 2), R_.encode_eps(ell * delta, dtype) + 2 * U) + 1e-14 * kap ** 2
         assert (np.abs(T[sent] - T_ref[sent]) <= eps_T * Mag[sent] + 1e-30).all(), p
         if ghat_d is not None:
             cols = [k * L + x for k in range(ell) for x in xs]

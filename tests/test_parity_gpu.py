@@ -207,7 +207,7 @@ def test_encode_and_reconstruct_parity(wl, ell, count):
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, Gw, ell)
     sent = psi > 0
     assert np.isnan(T[~sent]).all()
-    bound = R_.gamma(nterm)[:, :, None] * M
+    bound = R_.encode_bound(nterm, M, wl.g_dtype)
     diff = np.abs(T[sent].astype(np.float64) - T_ref[sent])
     assert (diff <= bound[sent]).all(), f"T off by {np.max(diff - bound[sent])}"
     # combine on identical inputs: the oracle's T rounded to fp32
@@ -292,7 +292,7 @@ def test_encode_worker_groups(wl, ell, count):
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, wl.g_dtype), ell)
     sent = psi > 0
     assert np.isnan(T[~sent]).all()
-    bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+    bound = R_.encode_bound(nterm, M, wl.g_dtype)[sent]
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
 
 
@@ -317,7 +317,7 @@ def test_encode_matrix_cores(wl, ell, count):
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, wl.g_dtype), ell)
     sent = psi > 0
     assert np.isnan(T[~sent]).all()
-    bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+    bound = R_.encode_bound(nterm, M, wl.g_dtype)[sent]
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
 
 
@@ -343,7 +343,7 @@ def _encode_against_oracle(O, order, psi, R, G, g_dtype, ell, d, shift=0):
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, OP.widen(G, g_dtype), ell)
     sent = psi > 0
     assert np.isnan(T[~sent]).all()
-    bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+    bound = R_.encode_bound(nterm, M, g_dtype)[sent]
     assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
 
 
@@ -382,6 +382,48 @@ def test_encode_matrix_rows_spilled_union():
     psi = g.integers(0, nu + 1, size=(2, m)).astype(np.int32)
     G = g.standard_normal((m, d)).astype(np.float32)
     _encode_against_oracle(O.astype(np.int64), order, psi, gen.shared_R(m, ell), G, "f32", ell, d)
+
+
+# bf16 chunk gradients past the all-chunk layout: the bf16 matrix cores, 32 rows of (pattern,
+# worker) per tile, coefficients split in three bf16 parts
+MX_WL = Workload(name="mx_m200_d4000_bf16", N=200, m=200, s=19, d=4000, P=40, ells=(1, 2, 4),
+                 g_dtype="bf16", pattern="uniform", forced_zero=30)
+MX_CASES = [
+    (MX_WL, 1, 1), (MX_WL, 1, 3), (MX_WL, 1, 8), (MX_WL, 2, 16), (MX_WL, 4, 33),
+    (dataclasses.replace(MX_WL, name="mx_m70_d4001_bf16", N=70, m=70, s=9, d=4001), 3, 8),   # ragged, 70 % 4
+    (dataclasses.replace(MX_WL, name="mx_m100_d81920_bf16", N=100, m=100, s=9, d=2048 * 40), 2, 5),
+    (dataclasses.replace(MX_WL, name="mx_m200_d1024_bf16", d=1024), 8, 4),    # too many rows: other path
+]
+
+
+@pytest.mark.parametrize("wl,ell,count", MX_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in MX_CASES])
+def test_encode_bf16_matrix_cores(wl, ell, count):
+    """bf16 gradients on the bf16 matrix cores: 1 to 33 patterns per call (32 / 8 / 4 / 2 / 1
+    workers per tile, two pattern tiles), ragged d and ell not dividing d (element-wise
+    staging), a group count that does not divide m, straggler rows untouched; and a shape
+    whose staged rows do not fit (ell = 8), which takes the worker-group path."""
+    O, order, _, _ = tables(wl)
+    _encode_against_oracle(O, order, patterns(wl, count), gen.shared_R(wl.m, ell), given_G(wl), "bf16",
+                           ell, wl.d)
+
+
+def test_encode_bf16_matrix_cores_misaligned_and_spilled_union():
+    """G one element off 16-byte alignment (element-wise staging); and a random 16-regular
+    support ordered by Algorithm 2, whose 8-worker groups use more chunks than their slots,
+    so each block walks its workers one at a time."""
+    import oracle.ordering as OO
+    wl = dataclasses.replace(MX_WL, name="mx_shift_m200_d4096_bf16", d=4096)
+    O, order, _, _ = tables(wl)
+    _encode_against_oracle(O, order, patterns(wl, 4), gen.shared_R(wl.m, 2), given_G(wl), "bf16", 2, wl.d,
+                           shift=1)
+    m, nu, d = 100, 16, 3000
+    A = gen.random_regular_graph(m, nu)
+    O2 = OO.chunk_ordering(A)
+    _, order2, _, _ = gcx.gc_assign(gcx.GC_ASSIGN_ORDER, m, m, -1, O2.astype(np.int32), nu, nu)
+    g = np.random.default_rng(43)
+    psi = g.integers(0, nu + 1, size=(4, m)).astype(np.int32)
+    G = gen.f32_to_bf16_bits(g.standard_normal((m, d)).astype(np.float32))
+    _encode_against_oracle(O2.astype(np.int64), order2, psi, gen.shared_R(m, 1), G, "bf16", 1, d)
 
 
 @pytest.mark.parametrize("wl,ell", [(TINY, 2), (GROUP_CASES[3][0], 2)], ids=["all-chunk", "worker-group"])
