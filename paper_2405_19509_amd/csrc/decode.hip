@@ -24,21 +24,15 @@ namespace {
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeWaves = kDecodeThreads / kWave;
 
+// One pattern by one wavefront, one lane per chunk: coverage, decodability, coefficient
+// error and the chunk's coefficients written straight to their (worker, position) slots.
 template <int ELL>
-__global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
-    const int32_t *__restrict__ psi, int64_t P, int N, int m, const int32_t *__restrict__ order,
-    int delta, const int32_t *__restrict__ holder, const int32_t *__restrict__ hpos, int gamma,
-    const float *__restrict__ R, int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
-    int32_t *__restrict__ coef_err, float *__restrict__ Bc) {
-  extern __shared__ float Rs[];  // [ELL][m]
-  if (R != nullptr)
-    for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
-  __syncthreads();  // the only barrier; every thread reaches it
-
-  const int lane = threadIdx.x % kWave;
-  const int64_t p = int64_t(blockIdx.x) * kDecodeWaves + threadIdx.x / kWave;
-  if (p >= P) return;
-
+__device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int64_t p, int N, int m,
+                                           const int32_t *__restrict__ order, int delta,
+                                           const int32_t *__restrict__ holder, const int32_t *__restrict__ hpos,
+                                           int gamma, const float *__restrict__ Rs, int32_t *__restrict__ cov,
+                                           uint8_t *__restrict__ dec, int32_t *__restrict__ coef_err,
+                                           float *__restrict__ Bc, int lane) {
   const int32_t *ps = psi + p * m;
   const int64_t wstride = int64_t(delta) * ELL;       // floats per worker in Bc
   const bool want_bc = Bc != nullptr;                  // else coverage only
@@ -204,6 +198,23 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
     dec[p] = invalid ? GC_DEC_INVALID : (ok ? GC_DEC_YES : GC_DEC_NO);
     coef_err[p] = err;
   }
+}
+
+template <int ELL>
+__global__ __launch_bounds__(kDecodeThreads) void decode_kernel(
+    const int32_t *__restrict__ psi, int64_t P, int N, int m, const int32_t *__restrict__ order,
+    int delta, const int32_t *__restrict__ holder, const int32_t *__restrict__ hpos, int gamma,
+    const float *__restrict__ R, int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
+    int32_t *__restrict__ coef_err, float *__restrict__ Bc) {
+  extern __shared__ float Rs[];  // [ELL][m]
+  if (R != nullptr)
+    for (int a = threadIdx.x; a < ELL * m; a += blockDim.x) Rs[a] = R[a];
+  __syncthreads();  // the only barrier; every thread reaches it
+
+  const int lane = threadIdx.x % kWave;
+  const int64_t p = int64_t(blockIdx.x) * kDecodeWaves + threadIdx.x / kWave;
+  if (p >= P) return;
+  decode_one<ELL>(psi, p, N, m, order, delta, holder, hpos, gamma, Rs, cov, dec, coef_err, Bc, lane);
 }
 
 // Two-phase variant, used whenever the assignment tables fit in LDS.  A persistent block
@@ -581,7 +592,202 @@ __attribute__((amdgpu_waves_per_eu(ELL <= 2 ? 8 : 1))) void decode_tiled_kernel(
   }
 }
 
+// ell = 1 with coefficients, N = m and gamma = delta: the cyclic assignment is checked
+// entry by entry on the device (chunk i held by worker (i - u) mod N at position u, worker j
+// holding chunk (j + t) mod N at position t) and, when it holds, each wave runs the
+// pattern with the tables replaced by index arithmetic.  psi and the squares R_j^2 are laid
+// out extended around the cycle (entry k holds worker (k - delta) mod N), so holder u of
+// chunk i sits at entry i - u + delta, and the reciprocals 1 / sum R^2 too (entry k holds
+// chunk k mod N), so position t of worker j reads entry j + t: no table reads, no modulo.
+// The arithmetic is the tiled kernel's (sum of R^2 over the holders in fp64, the
+// reciprocal, R_j times it in fp64, one rounding to fp32), with the holders summed in
+// ascending cyclic order (the tables' ascending worker order except for the chunks whose
+// holders wrap past worker N - 1).  Other tables: the one-phase path, per wave.
+//   LDS: R2x [m + delta] fp64, Rs [m] (+ pad); per wave F [N + delta] fp64, psi [m + delta].
+constexpr int kCycMaxWaves = 16;
+
+__host__ __device__ inline int64_t cyc_shared_bytes(int m, int delta) {
+  return ((8 * int64_t(m + delta) + 4 * int64_t(m)) + 15) & ~int64_t(15);
+}
+// per wave: the reciprocals F [N + delta] fp64 and psi extended [m + delta]
+__host__ __device__ inline int64_t cyc_wave_bytes(int N, int m, int delta) {
+  return ((8 * int64_t(N + delta) + 4 * int64_t(m + delta)) + 15) & ~int64_t(15);
+}
+
+__device__ __forceinline__ void decode_cyclic_l1(const int32_t *__restrict__ psi, int64_t p, int N, int delta,
+                                                 const double *__restrict__ R2x,
+                                                 const float *__restrict__ Rs, int32_t *pss, double *F,
+                                                 int32_t *__restrict__ cov, uint8_t *__restrict__ dec,
+                                                 int32_t *__restrict__ coef_err, float *__restrict__ Bc,
+                                                 int lane) {
+  const int m = N;
+  bool bad = false;
+  for (int j = lane; j < m; j += kWave) {
+    const int v = psi[p * m + j];
+    pss[j + delta] = v;
+    if (j >= m - delta) pss[j - (m - delta)] = v;
+    bad = bad || v < 0 || v > delta;
+  }
+  const bool invalid = __any(bad);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  // phase 1, one lane per chunk: coverage and the reciprocal of sum_{S_i} R^2
+  int err = 0;
+  bool all_ok = true;
+  for (int i = lane; i < N; i += kWave) {
+    int Delta = 0;
+    double ss = 0.0;
+    // holders in ascending cyclic order: worker i - delta + 1 + v (entry i + 1 + v) at
+    // position delta - 1 - v
+    const int32_t *pc = pss + i + 1;
+    const double *rc = R2x + i + 1;
+#pragma unroll 4
+    for (int v = 0; v < delta; ++v) {
+      const int pv = pc[v];
+      const double x2 = rc[v];
+      const bool member = pv > delta - 1 - v;
+      Delta += member ? 1 : 0;
+      ss += member ? x2 : 0.0;
+    }
+    if (cov != nullptr) cov[p * N + i] = Delta;
+    err += Delta < 1 ? 1 : 0;
+    all_ok = all_ok && Delta >= 1;
+    const double f = (invalid || Delta == 0) ? 0.0 : 1.0 / ss;
+    F[i] = f;
+    if (i < delta) F[i + N] = f;
+  }
+  err = wave_sum(err);
+  const bool ok = __all(all_ok);
+  if (lane == 0) {
+    dec[p] = invalid ? GC_DEC_INVALID : (ok ? GC_DEC_YES : GC_DEC_NO);
+    coef_err[p] = err;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  // phase 2, four consecutive coefficient rows per lane (worker j, positions t .. t + 3,
+  // reciprocals at F[j + t ..]); zero past the processed prefix.  A position inside the
+  // prefix always has a covered chunk (its own worker processed it), so its reciprocal is
+  // set; an invalid pattern writes zeros throughout (wave-uniform).
+  float *Bp = Bc + p * int64_t(m) * delta;
+  const int nrow = m * delta;
+  if (invalid) {
+    for (int e = lane; e < nrow; e += kWave) Bp[e] = 0.f;
+  } else if ((delta & 3) == 0 && (reinterpret_cast<uintptr_t>(Bp) & 15) == 0) {
+    int j4 = (4 * lane) / delta, t4 = (4 * lane) % delta;
+    const int j4_step = (4 * kWave) / delta, t4_step = (4 * kWave) % delta;
+    for (int e0 = 4 * lane; e0 < nrow; e0 += 4 * kWave) {
+      const double *fr = F + j4 + t4;
+      const int lim = pss[j4 + delta] - t4;  // positions t4 + q with q < lim are processed
+      const double r = Rs[j4];
+      float o[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = q < lim ? float(r * fr[q]) : 0.f;
+      *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
+      j4 += j4_step;
+      t4 += t4_step;
+      if (t4 >= delta) {
+        t4 -= delta;
+        ++j4;
+      }
+    }
+  } else {
+    int j = lane / delta, t = lane % delta;
+    const int j_step = kWave / delta, t_step = kWave % delta;
+    for (int e = lane; e < nrow; e += kWave) {
+      Bp[e] = pss[j + delta] > t ? float(double(Rs[j]) * F[j + t]) : 0.f;
+      j += j_step;
+      t += t_step;
+      if (t >= delta) {
+        t -= delta;
+        ++j;
+      }
+    }
+  }
+  // the next pattern overwrites this wave's arrays only after every lane is done with them
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(kCycMaxWaves * 64) __attribute__((amdgpu_waves_per_eu(8))) void
+decode_cyclic_l1_kernel(const int32_t *__restrict__ psi, int64_t P, int N, int m,
+                        const int32_t *__restrict__ order, int delta, const int32_t *__restrict__ holder,
+                        const int32_t *__restrict__ hpos, int gamma, const float *__restrict__ R,
+                        int32_t *__restrict__ cov, uint8_t *__restrict__ dec, int32_t *__restrict__ coef_err,
+                        float *__restrict__ Bc) {
+  extern __shared__ __align__(16) unsigned char lds_c[];
+  double *R2x = reinterpret_cast<double *>(lds_c);       // [m + delta]
+  float *Rs = reinterpret_cast<float *>(R2x + m + delta);  // [m]
+  // chunk i: its gamma = delta holders are the workers (i - t) mod N at positions t, in any
+  // order (gc_assign lists them by ascending worker)
+  bool cyc = N == m && gamma == delta && delta <= 64;
+  for (int i = threadIdx.x; i < N && cyc; i += blockDim.x) {
+    unsigned long long seen = 0;
+    for (int u = 0; u < gamma; ++u) {
+      const int j = holder[int64_t(i) * gamma + u], t = hpos[int64_t(i) * gamma + u];
+      const bool ok = t >= 0 && t < delta && j == (i - t + N) % N;
+      cyc = cyc && ok;
+      if (ok) seen |= 1ull << t;
+    }
+    cyc = cyc && seen == (delta == 64 ? ~0ull : (1ull << delta) - 1);
+  }
+  for (int e = threadIdx.x; e < m * delta; e += blockDim.x)
+    cyc = cyc && order[e] == (e / delta + e % delta) % N;
+  for (int k = threadIdx.x; k < m + delta; k += blockDim.x) {
+    const double x = double(R[((k - delta) % m + m) % m]);
+    R2x[k] = x * x;
+  }
+  for (int j = threadIdx.x; j < m; j += blockDim.x) Rs[j] = R[j];
+  const bool all_cyc = __syncthreads_and(cyc ? 1 : 0) != 0;  // the only block barrier
+
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;
+  unsigned char *region = lds_c + cyc_shared_bytes(m, delta) + size_t(wave) * cyc_wave_bytes(N, m, delta);
+  double *F = reinterpret_cast<double *>(region);                    // [N + delta]
+  int32_t *pss = reinterpret_cast<int32_t *>(F + N + delta);         // [m + delta]
+  for (int64_t p = int64_t(blockIdx.x) * nw + wave; p < P; p += int64_t(gridDim.x) * nw) {
+    if (all_cyc)
+      decode_cyclic_l1(psi, p, N, delta, R2x, Rs, pss, F, cov, dec, coef_err, Bc, lane);
+    else
+      decode_one<1>(psi, p, N, m, order, delta, holder, hpos, gamma, Rs, cov, dec, coef_err, Bc, lane);
+  }
+}
+
 constexpr size_t kDecodeLdsCU = 160 * 1024;  // LDS of one CU
+
+// the cyclic ell = 1 kernel when its LDS leaves at least 8 waves per CU; false otherwise
+bool launch_decode_cyclic_l1(const int32_t *psi, int64_t P, int N, int m, const int32_t *order, int delta,
+                             const int32_t *holder, const int32_t *hpos, int gamma, const float *R,
+                             int32_t *cov, uint8_t *dec, int32_t *coef_err, float *Bc, hipStream_t st,
+                             bool *launched) {
+  *launched = false;
+  const size_t shared = size_t(cyc_shared_bytes(m, delta)), per_wave = size_t(cyc_wave_bytes(N, m, delta));
+  int best_w = 0, best_total = 0;
+  for (int w = kCycMaxWaves; w >= 1; w >>= 1) {
+    const size_t lds = shared + w * per_wave;
+    if (lds > kDecodeLdsCU) continue;
+    const int per_cu = int(std::min<size_t>(kDecodeLdsCU / lds, 32 / w));
+    if (per_cu * w > best_total) {
+      best_total = per_cu * w;
+      best_w = w;
+    }
+  }
+  if (best_total < 8) return true;
+  const size_t lds = shared + best_w * per_wave;
+  const int64_t blocks = std::min(ceil_div(P, best_w), int64_t(best_total / best_w) * cu_count());
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute(reinterpret_cast<const void *>(&decode_cyclic_l1_kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
+    return false;
+  hipLaunchKernelGGL(decode_cyclic_l1_kernel, dim3(unsigned(blocks)), dim3(best_w * kWave), lds, st, psi, P,
+                     N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc);
+  *launched = true;
+  return true;
+}
 
 template <int ELL>
 bool launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *order, int delta,
@@ -589,6 +795,13 @@ bool launch_decode(const int32_t *psi, int64_t P, int N, int m, const int32_t *o
                    int32_t *cov, uint8_t *dec, int32_t *coef_err, float *Bc, hipStream_t st) {
   using Lay = DecodeLayout<ELL>;
   const bool bc = Bc != nullptr;
+  if (ELL == 1 && bc && N == m && gamma == delta) {
+    bool launched = false;
+    if (!launch_decode_cyclic_l1(psi, P, N, m, order, delta, holder, hpos, gamma, R, cov, dec, coef_err, Bc,
+                                 st, &launched))
+      return false;
+    if (launched) return true;
+  }
   const size_t shared = 4 * size_t(Lay::shared_words(N, m, gamma, delta, bc));
   const size_t per_wave = 4 * size_t(Lay::wave_words(N, m, bc));
   // the most waves per CU the LDS allows (at most 32), in blocks of up to 16 waves
