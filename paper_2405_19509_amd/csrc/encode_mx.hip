@@ -15,14 +15,16 @@
 // v_mfma_f32_32x32x16_bf16.  Error per output: at most u sum |a||g| from the split plus
 // the fp32 accumulation of 3 psi ell products, against psi ell for the vector path.
 //
-// Layout: a block owns a group of J consecutive workers, a tile of PB patterns
-// (J * PB = 32 rows (pattern, worker), row r = pb * J + jb) and a range of 512-wide
-// slices of x walked in turn.  Per slice it stages, straight from memory to LDS, the
-// slices of the group's union of chunks (J + delta - 1 chunks under the cyclic order),
-// one 1 KB row per (slot, block); the coefficient tile, split into its three bf16
-// planes, is built once per block.  Each of the 8 waves computes two 32 x 32 output
-// tiles per slice: per 16-deep K step three bf16x8 coefficient loads, eight 16-bit
-// gathers of the staged column per tile, six MFMAs.  Stores are 4 bytes per lane, two
+// Layout: a block owns a group of J consecutive workers, a window of PB patterns
+// (J * PB = 64 candidate rows (pattern, worker), candidate r = pb * J + jb) and a range of
+// 512-wide slices of x walked in turn.  The window's transmitting rows (psi > 0) are
+// compacted into one or two 32-row tiles (stragglers cost nothing), whose coefficients,
+// split into three bf16 planes, are built once per block.  Per slice the block stages,
+// straight from memory to LDS, the slices of the group's union of chunks (J + delta - 1
+// chunks under the cyclic order), one 1 KB row per (slot, block), and every row tile is
+// computed against them: each of the 8 waves takes two 32 x 32 output tiles per row tile,
+// per 16-deep K step three bf16x8 coefficient loads, eight 16-bit gathers of the staged
+// column per tile, six MFMAs.  Stores are 4 bytes per lane, two
 // 128-byte row segments per instruction, non-temporal; rows of workers that transmit
 // nothing (psi = 0) are not written.  Blocks of a slice range run back to back on one
 // XCD (round-robin dispatch), so its L2 serves the groups' overlapping chunk slices.
@@ -61,19 +63,19 @@ struct MxArgs {
   int m, delta, ell;
   float *T;
   bool stage16;   // G rows 16-byte aligned and d, L multiples of 8
-  int J;          // workers per tile
-  int PB;         // patterns per tile
+  int J;          // workers per window
+  int PB;         // patterns per window (J * PB = 64 candidate rows)
   int ngroups;
-  int64_t ntp;    // pattern tiles
+  int64_t ntp;    // pattern windows
   int slots;      // union slots staged per block
   int nslices;
   int64_t spb;    // slices per range
   int64_t nsr;    // slice ranges (a multiple of 8)
 };
 
-// LDS: [ Gs: Kp rows x kMxRowBytes ][ Ap: 3 planes x 32 rows x AP bf16 ][ rdesc: 2 int64 per row ]
-//      [ map: N int32 ][ slotc: slots int32 ][ code: J*delta int32 ]
-// The coefficient tile is first assembled in fp32 over the Gs region, then split into Ap.
+// LDS: [ Gs: Kp rows x kMxRowBytes ][ Ap: 2 tiles x 3 planes x 32 rows x AP bf16 ]
+//      [ rdesc: 2 int64 per row ][ map: N int32 ][ slotc: slots int32 ][ code: J*delta int32 ]
+// The coefficient rows are first assembled in fp32 over the Gs region, then split into Ap.
 template <int KS>
 __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4))) void encode_mx_kernel(MxArgs a) {
   constexpr int Kp = 16 * KS;
@@ -81,14 +83,14 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
   extern __shared__ __align__(16) unsigned char lds[];
   unsigned char *Gs = lds;
   uint16_t *Ap = reinterpret_cast<uint16_t *>(lds + size_t(Kp) * kMxRowBytes);
-  int64_t *rdesc = reinterpret_cast<int64_t *>(Ap + 3 * 32 * AP);
+  int64_t *rdesc = reinterpret_cast<int64_t *>(Ap + 2 * 3 * 32 * AP);
   int32_t *map = reinterpret_cast<int32_t *>(rdesc + 2 * Kp);
   int32_t *slotc = map + a.N;
   int32_t *code = slotc + a.slots;
-  float *Af = reinterpret_cast<float *>(Gs);  // [32][Kp] fp32, before the slices are staged
-  __shared__ int nslot_s, nuni_s;
-  __shared__ uint32_t rsend_s;
-  __shared__ int64_t rowoff_s[32];  // element offset of each tile row (pattern, worker) in T
+  float *Af = reinterpret_cast<float *>(Gs);  // [64][Kp] fp32, before the slices are staged
+  __shared__ int nslot_s, nuni_s, nsend_s;
+  __shared__ int8_t ccomp_s[64];    // compacted row of each candidate, or -1
+  __shared__ int64_t rowoff_s[64];  // element offset of each compacted row (pattern, worker) in T
 
   // block -> (slice range, unit = (group, pattern tile)); XCD x takes ranges x, x + 8, ...
   const int64_t b = blockIdx.x;
@@ -166,47 +168,53 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
       const int c = a.order[int64_t(j0 + jb) * a.delta + e % a.delta];
       code[e] = (jb >= ja && jb < jn && c >= 0 && c < a.N) ? map[c] : -1;
     }
-    for (int e = tid; e < 32 * Kp; e += kMxThreads) Af[e] = 0.f;
-    __syncthreads();
-    // the coefficient tile: row r = (pattern p0 + r / J, worker j0 + r % J), column
-    // s*ell + k; zero past each row's processed prefix
-    for (int e = tid; e < 32 * a.delta; e += kMxThreads) {
-      const int r = e / a.delta, t = e % a.delta;
-      const int pb = r / a.J, jb = r % a.J;
+    // the transmitting candidates of the pass, compacted in candidate order
+    if (tid < kWave) {
+      const int r = tid, pb = r / a.J, jb = r % a.J;
       const int64_t p = p0 + pb;
-      if (pb >= a.PB || p >= a.P || jb >= nj) continue;
+      const bool on = pb < a.PB && p < a.P && jb >= ja && jb < jn && a.psi[p * a.m + j0 + jb] > 0;
+      const unsigned long long mk = __ballot(on);
+      const int c = __popcll(mk & ((1ull << r) - 1));
+      ccomp_s[r] = on ? int8_t(c) : int8_t(-1);
+      if (on) rowoff_s[c] = (p * a.m + j0 + jb) * a.L;
+      if (tid == 0) nsend_s = __popcll(mk);
+    }
+    for (int e = tid; e < 64 * Kp; e += kMxThreads) Af[e] = 0.f;
+    __syncthreads();
+    const int nsend = nsend_s;
+    const int ntile = (nsend + 31) / 32;
+    // compacted row c (candidate (pattern p0 + r / J, worker j0 + r % J)), column s*ell + k:
+    // zero past the row's processed prefix
+    for (int e = tid; e < 64 * a.delta; e += kMxThreads) {
+      const int r = e / a.delta, t = e % a.delta;
+      const int c = ccomp_s[r];
+      if (c < 0) continue;
+      const int jb = r % a.J;
+      const int64_t p = p0 + r / a.J;
       const int s = code[jb * a.delta + t];
       if (s < 0) continue;
       int v = a.psi[p * a.m + j0 + jb];
       v = v < 0 ? 0 : (v > a.delta ? a.delta : v);
       if (t >= v) continue;
       const float *src = a.Bc + ((p * a.m + j0 + jb) * a.delta + t) * ell;
-      for (int k = 0; k < ell; ++k) Af[r * Kp + s * ell + k] = src[k];
-    }
-    if (tid < kWave) {
-      bool on = false;
-      if (tid < 32) {
-        const int pb = tid / a.J, jb = tid % a.J;
-        const int64_t p = p0 + pb;
-        if (pb < a.PB && p < a.P && jb >= ja && jb < jn) on = a.psi[p * a.m + j0 + jb] > 0;
-      }
-      const unsigned long long mk = __ballot(on);
-      if (tid == 0) rsend_s = uint32_t(mk);
-      if (tid < 32) rowoff_s[tid] = ((p0 + tid / a.J) * a.m + j0 + tid % a.J) * a.L;
+      for (int k = 0; k < ell; ++k) Af[c * Kp + s * ell + k] = src[k];
     }
     __syncthreads();
-    // three bf16 planes: a1 = bf16(a), a2 = bf16(a - a1), a3 = bf16(a - a1 - a2), all exact steps
-    for (int e = tid; e < 32 * Kp; e += kMxThreads) {
-      const int r = e / Kp, kk = e % Kp;
+    // three bf16 planes per row tile: a1 = bf16(a), a2 = bf16(a - a1), a3 = bf16(a - a1 - a2),
+    // all exact steps
+    for (int e = tid; e < 32 * ntile * Kp; e += kMxThreads) {
+      const int c = e / Kp, kk = e % Kp;
+      const int rt = c / 32, r = c % 32;
       const float v = Af[e];
       const uint32_t b1 = bf16_rne(v);
       const float r1 = v - __uint_as_float(b1 << 16);
       const uint32_t b2 = bf16_rne(r1);
       const float r2 = r1 - __uint_as_float(b2 << 16);
       const uint32_t b3 = bf16_rne(r2);
-      Ap[(0 * 32 + r) * AP + kk] = uint16_t(b1);
-      Ap[(1 * 32 + r) * AP + kk] = uint16_t(b2);
-      Ap[(2 * 32 + r) * AP + kk] = uint16_t(b3);
+      uint16_t *tp = Ap + rt * 3 * 32 * AP;
+      tp[(0 * 32 + r) * AP + kk] = uint16_t(b1);
+      tp[(1 * 32 + r) * AP + kk] = uint16_t(b2);
+      tp[(2 * 32 + r) * AP + kk] = uint16_t(b3);
     }
     // staged rows: element offset of block k of slot s's chunk, and the end of its valid
     // positions min(L, d - k L)
@@ -220,7 +228,7 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
     // rows K .. Kp of the slice region stay zero for the whole pass
     for (int e = tid; e < (Kp - K) * (kMxRowBytes / 16); e += kMxThreads)
       reinterpret_cast<uint4 *>(Gs + size_t(K) * kMxRowBytes)[e] = make_uint4(0u, 0u, 0u, 0u);
-    const uint32_t rsend = rsend_s;
+    if (ntile == 0) continue;  // nothing transmitted in this window: no slice to stage
 
     for (int64_t slice = s_begin; slice < s_end; ++slice) {
       const int64_t x0 = slice * kMxW;
@@ -247,38 +255,41 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
       __builtin_amdgcn_s_waitcnt(0);  // this wave's direct-to-LDS loads have landed
       __syncthreads();
 
-      // two 32 x 32 tiles per wave: positions x0 + 64 wave + 32 c + li
-      v16f acc0 = {}, acc1 = {};
+      // per row tile, two 32 x 32 tiles per wave: positions x0 + 64 wave + 32 c + li
       const uint16_t *Gc = reinterpret_cast<const uint16_t *>(Gs) + 64 * wave + li;
       constexpr int GR = kMxRowBytes / 2;  // staged row stride in bf16
+      for (int rt = 0; rt < ntile; ++rt) {
+        const uint16_t *At = Ap + rt * 3 * 32 * AP;
+        v16f acc0 = {}, acc1 = {};
 #pragma unroll 1
-      for (int q = 0; q < KS; ++q) {
-        const int kb = 16 * q + 8 * h;
-        const v8bf a1 = *reinterpret_cast<const v8bf *>(Ap + (0 * 32 + li) * AP + kb);
-        const v8bf a2 = *reinterpret_cast<const v8bf *>(Ap + (1 * 32 + li) * AP + kb);
-        const v8bf a3 = *reinterpret_cast<const v8bf *>(Ap + (2 * 32 + li) * AP + kb);
-        v8bf b0, b1;
+        for (int q = 0; q < KS; ++q) {
+          const int kb = 16 * q + 8 * h;
+          const v8bf a1 = *reinterpret_cast<const v8bf *>(At + (0 * 32 + li) * AP + kb);
+          const v8bf a2 = *reinterpret_cast<const v8bf *>(At + (1 * 32 + li) * AP + kb);
+          const v8bf a3 = *reinterpret_cast<const v8bf *>(At + (2 * 32 + li) * AP + kb);
+          v8bf b0, b1;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          b0[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR]);
-          b1[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR + 32]);
+          for (int i = 0; i < 8; ++i) {
+            b0[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR]);
+            b1[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR + 32]);
+          }
+          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b0, acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b1, acc1, 0, 0, 0);
+          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b0, acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b1, acc1, 0, 0, 0);
+          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc1, 0, 0, 0);
         }
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b1, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b1, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc1, 0, 0, 0);
-      }
-      // lane (h, li) holds D[8(v/4) + 4h + v%4][li] of each tile
+        // lane (h, li) holds D[8(v/4) + 4h + v%4][li] of each tile; compacted row c < nsend
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = 8 * (v >> 2) + 4 * h + (v & 3);
-        if (!((rsend >> r) & 1u)) continue;
-        float *row = a.T + rowoff_s[r];
-        const int64_t xa = x0 + 64 * wave + li, xb = xa + 32;
-        if (xa < a.L) __builtin_nontemporal_store(acc0[v], row + xa);
-        if (xb < a.L) __builtin_nontemporal_store(acc1[v], row + xb);
+        for (int v = 0; v < 16; ++v) {
+          const int c = rt * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+          if (c >= nsend) continue;
+          float *row = a.T + rowoff_s[c];
+          const int64_t xa = x0 + 64 * wave + li, xb = xa + 32;
+          if (xa < a.L) __builtin_nontemporal_store(acc0[v], row + xa);
+          if (xb < a.L) __builtin_nontemporal_store(acc1[v], row + xb);
+        }
       }
     }
   }
@@ -313,25 +324,31 @@ int encode_mx(const void *G, int32_t N, int64_t d, const int32_t *psi, const int
   a.ell = ell;
   a.T = T;
   a.stage16 = d % 8 == 0 && a.L % 8 == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0;
-  // 32 rows: PB patterns (a power of two covering the call, at most 32) x J workers
+  // up to 64 candidate rows: PB patterns (a power of two covering the call, at most 64) x J
+  // workers, J halved while the group's cyclic union would need more than kMxMaxKS K steps
   int pb = 1;
-  while (pb < 32 && pb < P) pb *= 2;
+  while (pb < 64 && pb < P) pb *= 2;
   a.PB = pb;
-  a.J = 32 / pb;
-  if (a.J > m) a.J = m;
-  a.ngroups = int(ceil_div(m, a.J));
-  a.ntp = ceil_div(P, pb);
   // slots for the cyclic union of a group; a block whose union is larger walks its workers
   // one at a time, each needing delta slots
-  int64_t slots = int64_t(a.J) + delta - 1;
-  if (slots > N) slots = N;
-  if (slots < delta) slots = delta;
+  auto union_slots = [&](int64_t J) {
+    int64_t sl = J + delta - 1;
+    if (sl > N) sl = N;
+    return sl < delta ? int64_t(delta) : sl;
+  };
+  int64_t J = 64 / pb;
+  if (J > m) J = m;
+  while (J > 1 && ceil_div(union_slots(J) * ell, 16) > kMxMaxKS) J /= 2;
+  a.J = int(J);
+  a.ngroups = int(ceil_div(m, a.J));
+  a.ntp = ceil_div(P, pb);
+  const int64_t slots = union_slots(J);
   a.slots = int(slots);
   const int64_t K = slots * ell;
   const int KS = int(ceil_div(K, 16));
   if (KS > kMxMaxKS) return kEncodeMxNotApplicable;
   const int Kp = 16 * KS;
-  const size_t lds = size_t(Kp) * kMxRowBytes + sizeof(uint16_t) * 3 * 32 * (Kp + 8) +
+  const size_t lds = size_t(Kp) * kMxRowBytes + sizeof(uint16_t) * 2 * 3 * 32 * (Kp + 8) +
                      2 * sizeof(int64_t) * size_t(Kp) + sizeof(int32_t) * (size_t(N) + slots + size_t(a.J) * delta);
   if (lds > kMxLds) return kEncodeMxNotApplicable;
   a.nslices = int(ceil_div(a.L, kMxW));
