@@ -71,6 +71,10 @@ def parse(argv=None):
                     help="skip timing the coefficients of the 100,000-pattern m = 200 workload")
     ap.add_argument("--no-direct", dest="direct", action="store_false",
                     help="skip timing gc_decode_direct (reported under 'direct', outside the step)")
+    ap.add_argument("--configs-only", choices=["given_m100_d1M", "given_m200_d16M_bf16", "decode_large"],
+                    default=None,
+                    help="profiling aid: run only this workload's configs (or the 100,000-pattern "
+                         "coefficients) and print their JSON, without the headline step")
     ap.add_argument("--copy-probe-mib", type=int, default=1024,
                     help="size of a plain device copy run once before warm-up (counter calibration)")
     return ap.parse_args(argv)
@@ -552,26 +556,30 @@ def large_batch(ell, override):
     return {1: 16, 2: 32, 4: 64}.get(ell, 16)
 
 
-def run_configs(gcx, args, dev, psi_large):
-    """The other workloads, outside the step."""
+def run_configs(gcx, args, dev, psi_large, only=None):
+    """The other workloads, outside the step (``only``: that one workload alone)."""
     import torch
     from workloads import BANDWIDTH, LARGE, SMALL, TINY, gen
     out = {}
-    for wl in (TINY, SMALL):
-        _log(f"{wl.name}: whole-step latency")
-        out[wl.name] = small_config_latency(gcx, wl, 1, dev)
+    if only is None:
+        for wl in (TINY, SMALL):
+            _log(f"{wl.name}: whole-step latency")
+            out[wl.name] = small_config_latency(gcx, wl, 1, dev)
     # m = 100, d = 2^20: all 10,000 patterns in batches
-    wl = BANDWIDTH
-    Gd = device_G(wl, dev)
-    gsum = gcx.gc_sum_chunks(Gd)
-    psi = gen.psi(wl)
-    rows = {}
-    for ell in ((1, 2, 8) if args.configs_full else (1, 2)):
-        batch = {1: 256, 2: 512, 8: 1024}[ell]
-        rows[f"exact_l{ell}"] = given_config(gcx, wl, ell, "exact", psi, Gd, gsum, batch, dev)
-    out[wl.name] = rows
-    del Gd, gsum
-    torch.cuda.empty_cache()
+    if only in (None, BANDWIDTH.name):
+        wl = BANDWIDTH
+        Gd = device_G(wl, dev)
+        gsum = gcx.gc_sum_chunks(Gd)
+        psi = gen.psi(wl)
+        rows = {}
+        for ell in ((1, 2, 8) if args.configs_full else (1, 2)):
+            batch = {1: 256, 2: 512, 8: 1024}[ell]
+            rows[f"exact_l{ell}"] = given_config(gcx, wl, ell, "exact", psi, Gd, gsum, batch, dev)
+        out[wl.name] = rows
+        del Gd, gsum
+        torch.cuda.empty_cache()
+    if only not in (None, LARGE.name):
+        return out
     # m = 200, d = 2^24, bf16: the first 1,000 patterns through encode and combine
     wl = LARGE
     Gd = device_G(wl, dev)
@@ -823,6 +831,25 @@ def experiment_shapes(args):
         torch.cuda.empty_cache()
 
 
+def configs_only(args):
+    """One workload's configs (or the 100,000-pattern coefficients) alone, for traces and
+    counters per workload; prints their JSON (not the bench line)."""
+    procs = min(CPU_PROCS_MAX, len(os.sched_getaffinity(0)))
+    large = args.configs_only in ("given_m200_d16M_bf16", "decode_large")
+    psi_large = large_patterns(procs) if large else None
+    import torch
+
+    from paper_2405_19509_amd import gcx
+    gcx.load()  # fail loudly if the HIP library is missing
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    if args.configs_only == "decode_large":
+        out = {"decode_large": time_decode_large(gcx, psi_large)}
+    else:
+        out = {"configs": run_configs(gcx, args, dev, psi_large, only=args.configs_only)}
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -837,6 +864,8 @@ def main():
         return experiment_ordering(args)
     if args.experiment == "shapes":
         return experiment_shapes(args)
+    if args.configs_only:
+        return configs_only(args)
 
     # ---- host work first, before the GPU is touched: the oracle baseline and the
     # 100,000 patterns of the m = 200 workload, both on forked worker processes ----

@@ -193,9 +193,14 @@ int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m, const 
  * [m][delta] int32 device; Bc [P][m][delta][ell] fp32 device (as from
  * gc_decode_coeffs); T [P][m][L] fp32 device.  fp32 accumulation.  psi is
  * clamped to [0, delta] and padded order slots are skipped.  G must be finite:
- * with 32 or more patterns per call and delta*ell >= 32 the sums run on the
- * matrix cores, where a coefficient past a pattern's prefix enters as zero (and
- * zero times a non-finite value is not zero).
+ * where the sums run on the matrix cores (bf16 G past the smallest shapes, fp32 G
+ * from delta*ell >= 32 terms), a coefficient past a pattern's prefix or of a chunk
+ * the worker does not hold enters as zero (and zero times a non-finite value is
+ * not zero).  Accuracy per output, M = sum over its terms of |Bc||g| and
+ * u = 2^-24: within u M plus the fp32 accumulation of 3 psi*ell products (bf16
+ * G; coefficients split exactly into three bf16 parts), within 8u M plus that of
+ * 6 psi*ell products (fp32 G on the matrix cores; G split exactly into three
+ * bf16 parts as well), or gamma_{psi*ell} M (fp32 vector path).
  */
 int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, const int32_t *psi,
               const int32_t *order, const float *Bc, int64_t P, int32_t m, int32_t delta,

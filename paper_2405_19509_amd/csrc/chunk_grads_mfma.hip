@@ -250,10 +250,25 @@ MfmaPlan mfma_plan(int N, int n, int64_t d, int b) {
   pl.mtiles1 = int(ceil_div(n, kTM));
   pl.ntiles1 = int(ceil_div(b, pl.tb));
   const int64_t tiles = int64_t(N) * pl.mtiles1 * pl.ntiles1;
-  int64_t splits = ceil_div(1536, tiles);  // about three waves of 2 blocks per CU on 256 CUs
-  if (splits < 1) splits = 1;
-  if (splits > 16) splits = 16;
-  int64_t kper = ceil_div(ceil_div(d, splits), kTK) * kTK;
+  // K = d split (at most 16 ways) so that the blocks fill whole rounds of the 512 resident
+  // ones (two per CU on 256 CUs): a grid that overshoots a round by a little runs its last
+  // round mostly empty.  Each split is charged half a percent (its Z partials, written and
+  // summed again, and a block prologue per tile); ties go to fewer splits.
+  constexpr int64_t kResident = 512;
+  int64_t splits = 1;
+  double best = -1.0;
+  for (int64_t sp = 1; sp <= 16; ++sp) {
+    const int64_t kp = ceil_div(ceil_div(d, sp), kTK) * kTK;
+    if (ceil_div(d, kp) != sp) continue;  // stage rounding merges splits: a smaller sp covers it
+    const int64_t blocks = tiles * sp;
+    const double fill = double(blocks) / double(ceil_div(blocks, kResident) * kResident);
+    const double score = fill - 0.005 * double(sp);
+    if (score > best + 1e-9) {
+      best = score;
+      splits = sp;
+    }
+  }
+  const int64_t kper = ceil_div(ceil_div(d, splits), kTK) * kTK;
   splits = ceil_div(d, kper);
   pl.splits = int(splits);
   pl.kper = kper;

@@ -239,12 +239,17 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
 // and are broadcast with readlane; the LDS offset of each term's slice comes from
 // a per-group table the same way.  The blocks of a slice run back to back on one
 // XCD, so its L2 serves the groups' overlapping chunk slices.
-// With a full 32-pattern tile per call and delta*ell >= 32 terms per output (a dense
-// contraction [32 patterns][terms] x [terms][128 positions] per worker), a block whose
-// group's chunks are all staged runs its items on the matrix cores instead
-// (v_mfma_f32_32x32x2f32; coefficients past a pattern's prefix enter as zeros, so the
-// gradient values must be finite).  With fewer patterns, the tile rows are 16 (pattern,
-// worker) pairs and its K the group's staged chunk blocks (v_mfma_f32_16x16x4f32).
+// Shapes with many terms per output normally take the bf16 matrix-core encode
+// (encode_mx.hip); where its staged rows do not fit, with a full 32-pattern tile per call
+// and delta*ell >= 32 terms per output (a dense contraction [32 patterns][terms] x
+// [terms][128 positions] per worker), a block whose group's chunks are all staged runs its
+// items on the fp32 matrix cores instead (v_mfma_f32_32x32x2f32; coefficients past a
+// pattern's prefix enter as zeros, so the gradient values must be finite).  With fewer
+// patterns, the tile rows are 16 (pattern, worker) pairs and its K the group's staged
+// chunk blocks (v_mfma_f32_16x16x4f32).
+// fp32 chunk gradients take the bf16 matrix-core encode from this many terms per output
+// (measured: at delta*ell = 20 the vector path writes as fast, at 80 the matrix cores win)
+constexpr int kMxF32Terms = 32;
 constexpr int kGrpThreads = 512;
 constexpr int kGrpWaves = kGrpThreads / kWave;
 constexpr size_t kGrpLds = 72 * 1024;     // per block: two blocks per CU
@@ -993,9 +998,10 @@ extern "C" int gc_encode(const void *G, int32_t g_dtype, int32_t N, int64_t d, c
   const int vec = (a.L % 4 == 0 && (ta & 15) == 0) ? 4 : ((a.L % 2 == 0 && (ta & 7) == 0) ? 2 : 1);
   const bool all_chunks = size_t(N) * ell * kWave * vec * esize <= kEncSliceLds;
   (void)hipGetLastError();
-  // bf16 chunk gradients beyond the all-chunk layout: the bf16 matrix cores, where they fit
-  if (g_dtype == GC_BF16 && !all_chunks) {
-    const int st = encode_mx(G, N, d, psi, order, Bc, P, m, delta, ell, T, stream);
+  // beyond the all-chunk layout, the bf16 matrix cores where they fit: always for bf16 chunk
+  // gradients; for fp32 ones from kMxF32Terms terms per output on
+  if (!all_chunks && (g_dtype == GC_BF16 || delta * ell >= kMxF32Terms)) {
+    const int st = encode_mx(G, g_dtype == GC_F32, N, d, psi, order, Bc, P, m, delta, ell, T, stream);
     if (st != kEncodeMxNotApplicable) return st != GC_OK ? st : launch_status();
   }
   const int st = g_dtype == GC_F32 ? dispatch_encode<float>(a, P, vec, all_chunks, stream)

@@ -1,4 +1,4 @@
-// gc_encode on the bf16 matrix cores, for bf16 chunk gradients (Sec. 2, worker encode):
+// gc_encode on the bf16 matrix cores (Sec. 2, worker encode):
 //   T[p][j][x] = sum_{t < psi[p][j]} sum_{k < ell} Bc[p][j][t][k] * g_{order[j][t]}[k*L + x]
 //
 // Why matrix cores: every output value of the encode takes psi*ell multiply-adds, 4-5 per
@@ -8,38 +8,47 @@
 // over kk = (chunk slot s of the group's union, block k), with A the coefficients of the
 // row's worker (zero where the worker does not hold the chunk or has not processed it).
 //
-// Arithmetic: the chunk gradients are bf16 already; each fp32 coefficient a is split
-// exactly into three bf16 parts a = a1 + a2 + a3 + r with |r| <= 2^-24 |a| (each part is
-// the bf16 rounding of what the previous ones leave), and the three products per term
-// (exact in fp32: 8 x 8 significant bits) are accumulated in fp32 by
-// v_mfma_f32_32x32x16_bf16.  Error per output: at most u sum |a||g| from the split plus
-// the fp32 accumulation of 3 psi ell products, against psi ell for the vector path.
+// Arithmetic: each fp32 coefficient a is split into three bf16 parts a = a1 + a2 + a3 + r
+// with |r| <= 2^-24 |a| (each part the bf16 rounding of what the previous ones leave).
+// bf16 chunk gradients enter as they are: three products per term.  An fp32 chunk gradient
+// g is split exactly into three bf16 parts by truncation (g1 its top 16 bits, g2 the top 16
+// bits of g - g1, g3 the rest), and the six products a_i g_j with i + j <= 4 are kept: the
+// dropped ones stay below 2^-21 |a g|.  Every product of two bf16 values is exact in fp32;
+// v_mfma_f32_32x32x16_bf16 accumulates them in fp32.
 //
 // Layout: a block owns a group of J consecutive workers, a window of PB patterns
 // (J * PB = 64 candidate rows (pattern, worker), candidate r = pb * J + jb) and a range of
-// 512-wide slices of x walked in turn.  The window's transmitting rows (psi > 0) are
-// compacted into one or two 32-row tiles (stragglers cost nothing), whose coefficients,
-// split into three bf16 planes, are built once per block.  Per slice the block stages,
-// straight from memory to LDS, the slices of the group's union of chunks (J + delta - 1
-// chunks under the cyclic order), one 1 KB row per (slot, block), and every row tile is
-// computed against them: each of the 8 waves takes two 32 x 32 output tiles per row tile,
-// per 16-deep K step three bf16x8 coefficient loads, eight 16-bit gathers of the staged
-// column per tile, six MFMAs.  Stores are 4 bytes per lane, two
-// 128-byte row segments per instruction, non-temporal; rows of workers that transmit
-// nothing (psi = 0) are not written.  Blocks of a slice range run back to back on one
-// XCD (round-robin dispatch), so its L2 serves the groups' overlapping chunk slices.
-// If a block's union exceeds its slots (orders other than the cyclic one), it walks its
-// workers one at a time (a pass per worker, each staging only that worker's chunks).
+// slices of x walked in turn.  The window's transmitting rows (psi > 0) are compacted into
+// one or two 32-row tiles (stragglers cost nothing), whose coefficients, split into three
+// bf16 planes, are built once per block.  Per slice the block stages the slices of the
+// group's union of chunks (J + delta - 1 chunks under the cyclic order), one row per (slot,
+// block), and every row tile is computed against them:
+//   bf16: 512-wide slices staged straight from memory to LDS (1 KB rows); each of the 8
+//         waves takes two 32 x 32 output tiles per row tile, per 16-deep K step three bf16x8
+//         coefficient loads, eight 16-bit gathers of the staged column per tile, six MFMAs;
+//   fp32: 256-wide slices staged through registers with the staged rows fastest, so that a
+//         lane's eight K values of one position are two 16-byte reads, split once per slice
+//         for both row tiles; each wave takes one 32-position tile, six MFMAs per row tile
+//         and K step.
+// Stores are 4 bytes per lane, two 128-byte row segments per instruction, non-temporal;
+// rows of workers that transmit nothing (psi = 0) are not written.  Blocks of a slice range
+// run back to back on one XCD (round-robin dispatch), so its L2 serves the groups'
+// overlapping chunk slices.  If a block's union exceeds its slots (orders other than the
+// cyclic one), it walks its workers one at a time (a pass per worker, each staging only
+// that worker's chunks).
+#include <type_traits>
+
 #include "common.h"
 #include "encode_mx.h"
 
 namespace gcx {
 namespace {
 
-constexpr int kMxThreads = 512;
-constexpr int kMxWaves = kMxThreads / kWave;
+constexpr int kMxThreads = 512;              // bf16, and fp32 with more than 3 K steps
 constexpr int kMxW = 512;                    // positions per slice (1 KB of bf16 per staged row)
 constexpr int kMxRowBytes = kMxW * 2 + 16;   // staged row stride: padded so rows 8 apart differ in bank
+constexpr int kMxfMaxWideKS = 3;             // fp32: 512-wide slices (1024 threads) up to 3 K steps
+static_assert(kMxW == (kMxThreads / 64) * 64 && kMxW * 2 == 64 * 16, "bf16: two 32-wide tiles per wave, 16 bytes per lane and staged row");
 constexpr int kMxMaxKS = 6;                  // K steps of 16 (at most 96 staged rows)
 constexpr size_t kMxLds = 152 * 1024;
 
@@ -52,8 +61,36 @@ __device__ __forceinline__ uint32_t bf16_rne(float v) {
   return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
 }
 
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+// Exact split of eight finite fp32 values into three bf16 parts each, g = g1 + g2 + g3:
+// g1 keeps the top 16 bits of g (sign, exponent, 7 fraction bits), g - g1 is exact with at
+// most 16 significant bits, g2 its top 16 bits, and what remains has at most 8 significant
+// bits, a bf16 value (|g2| < 2^-7 |g|, |g3| < 2^-15 |g|; exact for |g| >= 2^-100).
+__device__ __forceinline__ void split3(float4 u0, float4 u1, v8bf &g1, v8bf &g2, v8bf &g3) {
+  const float v[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+  uint32_t h1[8], h2[8], h3[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    h1[i] = __float_as_uint(v[i]) & 0xffff0000u;
+    const float r1 = v[i] - __uint_as_float(h1[i]);
+    h2[i] = __float_as_uint(r1) & 0xffff0000u;
+    h3[i] = __float_as_uint(r1 - __uint_as_float(h2[i]));
+  }
+  v4u p1, p2, p3;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {  // high halves: element 2j low, element 2j + 1 high
+    p1[j] = __builtin_amdgcn_perm(h1[2 * j + 1], h1[2 * j], 0x07060302u);
+    p2[j] = __builtin_amdgcn_perm(h2[2 * j + 1], h2[2 * j], 0x07060302u);
+    p3[j] = __builtin_amdgcn_perm(h3[2 * j + 1], h3[2 * j], 0x07060302u);
+  }
+  g1 = __builtin_bit_cast(v8bf, p1);
+  g2 = __builtin_bit_cast(v8bf, p2);
+  g3 = __builtin_bit_cast(v8bf, p3);
+}
+
 struct MxArgs {
-  const uint16_t *G;
+  const void *G;
   int N;
   int64_t d, L;
   const int32_t *psi;
@@ -62,7 +99,7 @@ struct MxArgs {
   int64_t P;
   int m, delta, ell;
   float *T;
-  bool stage16;   // G rows 16-byte aligned and d, L multiples of 8
+  bool stage16;   // bf16: G 16-byte aligned and d, L multiples of 8; fp32: 8-byte, multiples of 2
   int J;          // workers per window
   int PB;         // patterns per window (J * PB = 64 candidate rows)
   int ngroups;
@@ -73,16 +110,38 @@ struct MxArgs {
   int64_t nsr;    // slice ranges (a multiple of 8)
 };
 
-// LDS: [ Gs: Kp rows x kMxRowBytes ][ Ap: 2 tiles x 3 planes x 32 rows x AP bf16 ]
+// Slice region of the LDS, by chunk-gradient type:
+//   bf16: Kp staged rows x kMxRowBytes, position fastest (filled straight from memory)
+//   fp32: W positions x (Kp + 4) floats, staged row fastest (a lane's eight K values of
+//         one position are two 16-byte reads)
+template <typename GT, int KS>
+struct MxLayout {
+  static constexpr bool F32 = sizeof(GT) == 4;
+  static constexpr int Kp = 16 * KS;
+  // fp32: one 32-wide tile per wave, 2 KB row segments of T per slice (16 waves) while the
+  // staged rows fit, else 256 positions (8 waves); bf16: two tiles per wave, 512 positions
+  static constexpr int THREADS = F32 && KS <= kMxfMaxWideKS ? 1024 : kMxThreads;
+  static constexpr int WAVES = THREADS / 64;
+  static constexpr int W = F32 ? 32 * WAVES : kMxW;  // positions per slice
+  static constexpr int BS = Kp + 4;                  // fp32: floats per staged position
+  static constexpr size_t slice_bytes = F32 ? size_t(W) * BS * 4 : size_t(Kp) * kMxRowBytes;
+  static_assert(!F32 || (W / 2) % 128 == 0, "fp32 staging: two positions per thread, whole waves per row group");
+};
+
+// LDS: [ slice region ][ Ap: 2 tiles x 3 planes x 32 rows x AP bf16 ]
 //      [ rdesc: 2 int64 per row ][ map: N int32 ][ slotc: slots int32 ][ code: J*delta int32 ]
-// The coefficient rows are first assembled in fp32 over the Gs region, then split into Ap.
-template <int KS>
-__global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4))) void encode_mx_kernel(MxArgs a) {
-  constexpr int Kp = 16 * KS;
+// The coefficient rows are first assembled in fp32 over the slice region, then split into Ap.
+template <typename GT, int KS>
+__global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_waves_per_eu(4))) void encode_mx_kernel(
+    MxArgs a) {
+  using Lay = MxLayout<GT, KS>;
+  constexpr int NTH = Lay::THREADS;
+  constexpr bool F32 = Lay::F32;
+  constexpr int Kp = Lay::Kp;
   constexpr int AP = Kp + 8;  // plane row stride (bf16): 16-byte aligned rows, staggered banks
   extern __shared__ __align__(16) unsigned char lds[];
   unsigned char *Gs = lds;
-  uint16_t *Ap = reinterpret_cast<uint16_t *>(lds + size_t(Kp) * kMxRowBytes);
+  uint16_t *Ap = reinterpret_cast<uint16_t *>(lds + Lay::slice_bytes);
   int64_t *rdesc = reinterpret_cast<int64_t *>(Ap + 2 * 3 * 32 * AP);
   int32_t *map = reinterpret_cast<int32_t *>(rdesc + 2 * Kp);
   int32_t *slotc = map + a.N;
@@ -90,7 +149,9 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
   float *Af = reinterpret_cast<float *>(Gs);  // [64][Kp] fp32, before the slices are staged
   __shared__ int nslot_s, nuni_s, nsend_s;
   __shared__ int8_t ccomp_s[64];    // compacted row of each candidate, or -1
-  __shared__ int64_t rowoff_s[64];  // element offset of each compacted row (pattern, worker) in T
+  // each compacted row's element offset in T from the window's first row (pattern p0,
+  // worker j0): (pb * m + jb) * L; read two at a time by the stores
+  __shared__ __align__(16) int64_t rowoff_s[64];
 
   // block -> (slice range, unit = (group, pattern tile)); XCD x takes ranges x, x + 8, ...
   const int64_t b = blockIdx.x;
@@ -105,14 +166,15 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
   const int j0 = gi * a.J;
   const int nj = a.m - j0 < a.J ? a.m - j0 : a.J;
   const int ell = a.ell;
+  float *const Tw = a.T + (p0 * a.m + j0) * a.L;  // row (pattern p0, worker j0) of T
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave, h = lane >> 5, li = lane & 31;
 
   // which chunks the whole group uses; if they exceed the slots, one worker per pass
-  for (int c = tid; c < a.N; c += kMxThreads) map[c] = 0;
+  for (int c = tid; c < a.N; c += NTH) map[c] = 0;
   __syncthreads();
-  for (int e = tid; e < nj * a.delta; e += kMxThreads) {
+  for (int e = tid; e < nj * a.delta; e += NTH) {
     const int c = a.order[int64_t(j0) * a.delta + e];
     if (c >= 0 && c < a.N) map[c] = 1;
   }
@@ -134,9 +196,9 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
     // active workers of this pass: all nj, or worker jb = pass
     const int ja = split ? pass : 0, jn = split ? pass + 1 : nj;
     __syncthreads();  // the previous pass is done with every table
-    for (int c = tid; c < a.N; c += kMxThreads) map[c] = 0;
+    for (int c = tid; c < a.N; c += NTH) map[c] = 0;
     __syncthreads();
-    for (int e = tid; e < (jn - ja) * a.delta; e += kMxThreads) {
+    for (int e = tid; e < (jn - ja) * a.delta; e += NTH) {
       const int c = a.order[int64_t(j0 + ja) * a.delta + e];
       if (c >= 0 && c < a.N) map[c] = 1;
     }
@@ -163,7 +225,7 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
     const int nslot = nslot_s;
     const int K = nslot * ell;
     // per (worker, position): the slot of the chunk there, or -1
-    for (int e = tid; e < nj * a.delta; e += kMxThreads) {
+    for (int e = tid; e < nj * a.delta; e += NTH) {
       const int jb = e / a.delta;
       const int c = a.order[int64_t(j0 + jb) * a.delta + e % a.delta];
       code[e] = (jb >= ja && jb < jn && c >= 0 && c < a.N) ? map[c] : -1;
@@ -176,16 +238,16 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
       const unsigned long long mk = __ballot(on);
       const int c = __popcll(mk & ((1ull << r) - 1));
       ccomp_s[r] = on ? int8_t(c) : int8_t(-1);
-      if (on) rowoff_s[c] = (p * a.m + j0 + jb) * a.L;
+      if (on) rowoff_s[c] = (int64_t(pb) * a.m + jb) * a.L;
       if (tid == 0) nsend_s = __popcll(mk);
     }
-    for (int e = tid; e < 64 * Kp; e += kMxThreads) Af[e] = 0.f;
+    for (int e = tid; e < 64 * Kp; e += NTH) Af[e] = 0.f;
     __syncthreads();
     const int nsend = nsend_s;
     const int ntile = (nsend + 31) / 32;
     // compacted row c (candidate (pattern p0 + r / J, worker j0 + r % J)), column s*ell + k:
     // zero past the row's processed prefix
-    for (int e = tid; e < 64 * a.delta; e += kMxThreads) {
+    for (int e = tid; e < 64 * a.delta; e += NTH) {
       const int r = e / a.delta, t = e % a.delta;
       const int c = ccomp_s[r];
       if (c < 0) continue;
@@ -202,7 +264,7 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
     __syncthreads();
     // three bf16 planes per row tile: a1 = bf16(a), a2 = bf16(a - a1), a3 = bf16(a - a1 - a2),
     // all exact steps
-    for (int e = tid; e < 32 * ntile * Kp; e += kMxThreads) {
+    for (int e = tid; e < 32 * ntile * Kp; e += NTH) {
       const int c = e / Kp, kk = e % Kp;
       const int rt = c / 32, r = c % 32;
       const float v = Af[e];
@@ -218,100 +280,215 @@ __global__ __launch_bounds__(kMxThreads) __attribute__((amdgpu_waves_per_eu(4)))
     }
     // staged rows: element offset of block k of slot s's chunk, and the end of its valid
     // positions min(L, d - k L)
-    for (int row = tid; row < K; row += kMxThreads) {
+    for (int row = tid; row < K; row += NTH) {
       const int s = row / ell, k = row % ell;
       rdesc[2 * row] = int64_t(slotc[s]) * a.d + int64_t(k) * a.L;
       const int64_t rem = a.d - int64_t(k) * a.L;
       rdesc[2 * row + 1] = rem < a.L ? rem : a.L;
     }
     __syncthreads();  // Af consumed: the slice region is free
-    // rows K .. Kp of the slice region stay zero for the whole pass
-    for (int e = tid; e < (Kp - K) * (kMxRowBytes / 16); e += kMxThreads)
-      reinterpret_cast<uint4 *>(Gs + size_t(K) * kMxRowBytes)[e] = make_uint4(0u, 0u, 0u, 0u);
+    // bf16: rows K .. Kp of the slice region stay zero for the whole pass (fp32: the
+    // staging writes them)
+    if constexpr (!F32)
+      for (int e = tid; e < (Kp - K) * (kMxRowBytes / 16); e += NTH)
+        reinterpret_cast<uint4 *>(Gs + size_t(K) * kMxRowBytes)[e] = make_uint4(0u, 0u, 0u, 0u);
     if (ntile == 0) continue;  // nothing transmitted in this window: no slice to stage
 
     for (int64_t slice = s_begin; slice < s_end; ++slice) {
-      const int64_t x0 = slice * kMxW;
+      const int64_t x0 = slice * Lay::W;
       __syncthreads();  // the previous slice is consumed
-      // stage: staged row `row` <- 512 positions of its block from x0 (zero past L or d);
-      // one wave instruction per row, lane i filling bytes 16i..16i+15 of its 1 KB
-      for (int row = wave; row < K; row += kMxWaves) {
-        const int64_t base = rdesc[2 * row], lim = rdesc[2 * row + 1];
-        const int64_t x = x0 + 8 * lane;
-        unsigned char *dst = Gs + size_t(row) * kMxRowBytes;
-        if (a.stage16 && x0 + kMxW <= lim) {
-          __builtin_amdgcn_global_load_lds(a.G + base + x, dst, 16, 0, 0);
-        } else {
-          uint32_t w[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const uint32_t lo = x + 2 * q < lim ? a.G[base + x + 2 * q] : 0u;
-            const uint32_t hi = x + 2 * q + 1 < lim ? a.G[base + x + 2 * q + 1] : 0u;
-            w[q] = lo | (hi << 16);
-          }
-          *reinterpret_cast<uint4 *>(dst + 16 * lane) = make_uint4(w[0], w[1], w[2], w[3]);
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(0);  // this wave's direct-to-LDS loads have landed
-      __syncthreads();
-
-      // per row tile, two 32 x 32 tiles per wave: positions x0 + 64 wave + 32 c + li
-      const uint16_t *Gc = reinterpret_cast<const uint16_t *>(Gs) + 64 * wave + li;
-      constexpr int GR = kMxRowBytes / 2;  // staged row stride in bf16
-      for (int rt = 0; rt < ntile; ++rt) {
-        const uint16_t *At = Ap + rt * 3 * 32 * AP;
-        v16f acc0 = {}, acc1 = {};
+      if constexpr (F32) {
+        // stage: a thread takes positions xp, xp + 1 and groups of 8 staged rows, and writes
+        // each position's 8 values as two 16-byte words (zero past L, d or K)
+        float *Bf = reinterpret_cast<float *>(Gs);
+        const float *Gf = static_cast<const float *>(a.G);
+        const int xp = 2 * (tid % (Lay::W / 2));
+        const int64_t x = x0 + xp;
 #pragma unroll 1
-        for (int q = 0; q < KS; ++q) {
-          const int kb = 16 * q + 8 * h;
-          const v8bf a1 = *reinterpret_cast<const v8bf *>(At + (0 * 32 + li) * AP + kb);
-          const v8bf a2 = *reinterpret_cast<const v8bf *>(At + (1 * 32 + li) * AP + kb);
-          const v8bf a3 = *reinterpret_cast<const v8bf *>(At + (2 * 32 + li) * AP + kb);
-          v8bf b0, b1;
+        for (int g = tid / (Lay::W / 2); g < Kp / 8; g += (NTH / (Lay::W / 2))) {
+          float v0[8], v1[8];
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
-            b0[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR]);
-            b1[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR + 32]);
+            const int kk = 8 * g + i;
+            v0[i] = 0.f;
+            v1[i] = 0.f;
+            if (kk < K) {
+              const int64_t base = rdesc[2 * kk], lim = rdesc[2 * kk + 1];
+              if (a.stage16 && x + 2 <= lim) {
+                const float2 u = *reinterpret_cast<const float2 *>(Gf + base + x);
+                v0[i] = u.x;
+                v1[i] = u.y;
+              } else {
+                if (x < lim) v0[i] = Gf[base + x];
+                if (x + 1 < lim) v1[i] = Gf[base + x + 1];
+              }
+            }
           }
-          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b0, acc0, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b1, acc1, 0, 0, 0);
-          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b0, acc0, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b1, acc1, 0, 0, 0);
-          acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc0, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc1, 0, 0, 0);
+          float *d0 = Bf + xp * Lay::BS + 8 * g, *d1 = d0 + Lay::BS;
+          *reinterpret_cast<float4 *>(d0) = make_float4(v0[0], v0[1], v0[2], v0[3]);
+          *reinterpret_cast<float4 *>(d0 + 4) = make_float4(v0[4], v0[5], v0[6], v0[7]);
+          *reinterpret_cast<float4 *>(d1) = make_float4(v1[0], v1[1], v1[2], v1[3]);
+          *reinterpret_cast<float4 *>(d1 + 4) = make_float4(v1[4], v1[5], v1[6], v1[7]);
         }
-        // lane (h, li) holds D[8(v/4) + 4h + v%4][li] of each tile; compacted row c < nsend
+      } else {
+        // stage: staged row `row` <- 512 positions of its block from x0 (zero past L or d),
+        // straight from memory to LDS: one wave instruction per row, lane i filling bytes
+        // 16i .. 16i + 15 of its 1 KB
+        const uint16_t *Gh = static_cast<const uint16_t *>(a.G);
+        for (int row = wave; row < K; row += Lay::WAVES) {
+          const int64_t base = rdesc[2 * row], lim = rdesc[2 * row + 1];
+          const int64_t x = x0 + 8 * lane;
+          unsigned char *dst = Gs + size_t(row) * kMxRowBytes;
+          if (a.stage16 && x0 + kMxW <= lim) {
+            __builtin_amdgcn_global_load_lds(Gh + base + x, dst, 16, 0, 0);
+          } else {
+            uint32_t w[4];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int c = rt * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-          if (c >= nsend) continue;
-          float *row = a.T + rowoff_s[c];
+            for (int q = 0; q < 4; ++q) {
+              const uint32_t lo = x + 2 * q < lim ? Gh[base + x + 2 * q] : 0u;
+              const uint32_t hi = x + 2 * q + 1 < lim ? Gh[base + x + 2 * q + 1] : 0u;
+              w[q] = lo | (hi << 16);
+            }
+            *reinterpret_cast<uint4 *>(dst + 16 * lane) = make_uint4(w[0], w[1], w[2], w[3]);
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's direct-to-LDS loads have landed
+      }
+      __syncthreads();  // the slice is staged
+
+      if constexpr (F32) {
+        // one 32-position tile per wave (x0 + 32 wave + li), every row tile in one K loop so
+        // that each staged value is split once
+        const float *Bw = reinterpret_cast<const float *>(Gs) + (32 * wave + li) * Lay::BS + 8 * h;
+        auto tiles = [&](auto ntc) {
+          constexpr int NT = decltype(ntc)::value;
+          v16f acc[NT];
+#pragma unroll
+          for (int t = 0; t < NT; ++t) acc[t] = v16f{};
+#pragma unroll 1
+          for (int q = 0; q < KS; ++q) {
+            const float4 u0 = *reinterpret_cast<const float4 *>(Bw + 16 * q);
+            const float4 u1 = *reinterpret_cast<const float4 *>(Bw + 16 * q + 4);
+            v8bf g1, g2, g3;
+            split3(u0, u1, g1, g2, g3);
+            const int kb = 16 * q + 8 * h;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+              const uint16_t *At = Ap + t * 3 * 32 * AP;
+              const v8bf a1 = *reinterpret_cast<const v8bf *>(At + (0 * 32 + li) * AP + kb);
+              const v8bf a2 = *reinterpret_cast<const v8bf *>(At + (1 * 32 + li) * AP + kb);
+              const v8bf a3 = *reinterpret_cast<const v8bf *>(At + (2 * 32 + li) * AP + kb);
+              // the six products of parts above 2^-24 relative, smallest first
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, g1, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, g2, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, g3, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, g1, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, g2, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, g1, acc[t], 0, 0, 0);
+            }
+          }
+          const int64_t xa = x0 + 32 * wave + li;
+          if (xa >= a.L) return;
+          // lane (h, li) holds D[8(v/4) + 4h + v%4][li]: rows 32t + 8g + 4h + i, their
+          // offsets read four at a time (two 16-byte reads)
+          float *Tx = Tw + xa;
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int cb = 32 * t + 8 * g + 4 * h;
+              const longlong2 o0 = *reinterpret_cast<const longlong2 *>(rowoff_s + cb);
+              const longlong2 o1 = *reinterpret_cast<const longlong2 *>(rowoff_s + cb + 2);
+              const int64_t off[4] = {o0.x, o0.y, o1.x, o1.y};
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                if (cb + i < nsend) __builtin_nontemporal_store(acc[t][4 * g + i], Tx + off[i]);
+            }
+        };
+        if (ntile == 2)
+          tiles(std::integral_constant<int, 2>{});
+        else
+          tiles(std::integral_constant<int, 1>{});
+      } else {
+        // per row tile, two 32 x 32 tiles per wave: positions x0 + 64 wave + 32 c + li
+        const uint16_t *Gc = reinterpret_cast<const uint16_t *>(Gs) + 64 * wave + li;
+        constexpr int GR = kMxRowBytes / 2;  // staged row stride in bf16
+        for (int rt = 0; rt < ntile; ++rt) {
+          const uint16_t *At = Ap + rt * 3 * 32 * AP;
+          v16f acc0 = {}, acc1 = {};
+#pragma unroll 1
+          for (int q = 0; q < KS; ++q) {
+            const int kb = 16 * q + 8 * h;
+            const v8bf a1 = *reinterpret_cast<const v8bf *>(At + (0 * 32 + li) * AP + kb);
+            const v8bf a2 = *reinterpret_cast<const v8bf *>(At + (1 * 32 + li) * AP + kb);
+            const v8bf a3 = *reinterpret_cast<const v8bf *>(At + (2 * 32 + li) * AP + kb);
+            v8bf b0, b1;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              b0[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR]);
+              b1[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR + 32]);
+            }
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b0, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, b1, acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b0, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b1, acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc1, 0, 0, 0);
+          }
+          // lane (h, li) holds D[8(v/4) + 4h + v%4][li] of each tile: rows 32 rt + 8g + 4h +
+          // i, their offsets read four at a time (two 16-byte reads)
           const int64_t xa = x0 + 64 * wave + li, xb = xa + 32;
-          if (xa < a.L) __builtin_nontemporal_store(acc0[v], row + xa);
-          if (xb < a.L) __builtin_nontemporal_store(acc1[v], row + xb);
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int cb = 32 * rt + 8 * g + 4 * h;
+            const longlong2 o0 = *reinterpret_cast<const longlong2 *>(rowoff_s + cb);
+            const longlong2 o1 = *reinterpret_cast<const longlong2 *>(rowoff_s + cb + 2);
+            const int64_t off[4] = {o0.x, o0.y, o1.x, o1.y};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if (cb + i >= nsend) continue;
+              float *row = Tw + off[i];
+              if (xa < a.L) __builtin_nontemporal_store(acc0[4 * g + i], row + xa);
+              if (xb < a.L) __builtin_nontemporal_store(acc1[4 * g + i], row + xb);
+            }
+          }
         }
       }
     }
   }
 }
 
-template <int KS>
+template <typename GT, int KS>
 int launch_mx_ks(const MxArgs &m, size_t lds, hipStream_t st) {
   const int64_t blocks = m.nsr * m.ngroups * m.ntp;
-  if (!grid_ok(blocks, kMxThreads)) return GC_EINVAL;
-  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_mx_kernel<KS>),
+  constexpr int NTH = MxLayout<GT, KS>::THREADS;
+  if (!grid_ok(blocks, NTH)) return GC_EINVAL;
+  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_mx_kernel<GT, KS>),
                           hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
     return GC_ELAUNCH;
-  hipLaunchKernelGGL((encode_mx_kernel<KS>), dim3(unsigned(blocks)), dim3(kMxThreads), lds, st, m);
+  hipLaunchKernelGGL((encode_mx_kernel<GT, KS>), dim3(unsigned(blocks)), dim3(NTH), lds, st, m);
   return GC_OK;
+}
+
+template <typename GT>
+int launch_mx(const MxArgs &a, int KS, size_t lds, hipStream_t st) {
+  switch (KS) {
+    case 1: return launch_mx_ks<GT, 1>(a, lds, st);
+    case 2: return launch_mx_ks<GT, 2>(a, lds, st);
+    case 3: return launch_mx_ks<GT, 3>(a, lds, st);
+    case 4: return launch_mx_ks<GT, 4>(a, lds, st);
+    case 5: return launch_mx_ks<GT, 5>(a, lds, st);
+    case 6: return launch_mx_ks<GT, 6>(a, lds, st);
+    default: return kEncodeMxNotApplicable;
+  }
 }
 
 }  // namespace
 
-int encode_mx(const void *G, int32_t N, int64_t d, const int32_t *psi, const int32_t *order, const float *Bc,
-              int64_t P, int32_t m, int32_t delta, int32_t ell, float *T, hipStream_t stream) {
+int encode_mx(const void *G, bool f32, int32_t N, int64_t d, const int32_t *psi, const int32_t *order,
+              const float *Bc, int64_t P, int32_t m, int32_t delta, int32_t ell, float *T, hipStream_t stream) {
   MxArgs a{};
-  a.G = static_cast<const uint16_t *>(G);
+  a.G = G;
   a.N = N;
   a.d = d;
   a.L = ceil_div(d, ell);
@@ -323,7 +500,8 @@ int encode_mx(const void *G, int32_t N, int64_t d, const int32_t *psi, const int
   a.delta = delta;
   a.ell = ell;
   a.T = T;
-  a.stage16 = d % 8 == 0 && a.L % 8 == 0 && (reinterpret_cast<uintptr_t>(G) & 15) == 0;
+  const uintptr_t ga = reinterpret_cast<uintptr_t>(G);
+  a.stage16 = f32 ? (d % 2 == 0 && a.L % 2 == 0 && (ga & 7) == 0) : (d % 8 == 0 && a.L % 8 == 0 && (ga & 15) == 0);
   // up to 64 candidate rows: PB patterns (a power of two covering the call, at most 64) x J
   // workers, J halved while the group's cyclic union would need more than kMxMaxKS K steps
   int pb = 1;
@@ -348,10 +526,12 @@ int encode_mx(const void *G, int32_t N, int64_t d, const int32_t *psi, const int
   const int KS = int(ceil_div(K, 16));
   if (KS > kMxMaxKS) return kEncodeMxNotApplicable;
   const int Kp = 16 * KS;
-  const size_t lds = size_t(Kp) * kMxRowBytes + sizeof(uint16_t) * 2 * 3 * 32 * (Kp + 8) +
-                     2 * sizeof(int64_t) * size_t(Kp) + sizeof(int32_t) * (size_t(N) + slots + size_t(a.J) * delta);
+  const int W = f32 ? (KS <= kMxfMaxWideKS ? 512 : 256) : kMxW;
+  const size_t slice = f32 ? size_t(W) * (Kp + 4) * sizeof(float) : size_t(Kp) * kMxRowBytes;
+  const size_t lds = slice + sizeof(uint16_t) * 2 * 3 * 32 * (Kp + 8) + 2 * sizeof(int64_t) * size_t(Kp) +
+                     sizeof(int32_t) * (size_t(N) + slots + size_t(a.J) * delta);
   if (lds > kMxLds) return kEncodeMxNotApplicable;
-  a.nslices = int(ceil_div(a.L, kMxW));
+  a.nslices = int(ceil_div(a.L, W));
   // slice ranges: a multiple of 8 (one share per XCD), about 16 blocks per CU in all
   const int64_t units = int64_t(a.ngroups) * a.ntp;
   const int64_t want = 16 * int64_t(cu_count());
@@ -359,15 +539,7 @@ int encode_mx(const void *G, int32_t N, int64_t d, const int32_t *psi, const int
   if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
   a.spb = ceil_div(a.nslices, nsr);
   a.nsr = ceil_div(ceil_div(a.nslices, a.spb), 8) * 8;
-  switch (KS) {
-    case 1: return launch_mx_ks<1>(a, lds, stream);
-    case 2: return launch_mx_ks<2>(a, lds, stream);
-    case 3: return launch_mx_ks<3>(a, lds, stream);
-    case 4: return launch_mx_ks<4>(a, lds, stream);
-    case 5: return launch_mx_ks<5>(a, lds, stream);
-    case 6: return launch_mx_ks<6>(a, lds, stream);
-    default: return kEncodeMxNotApplicable;
-  }
+  return f32 ? launch_mx<float>(a, KS, lds, stream) : launch_mx<uint16_t>(a, KS, lds, stream);
 }
 
 }  // namespace gcx

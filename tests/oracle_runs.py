@@ -23,22 +23,28 @@ def gamma(n):
 
 def encode_bound(nterm, M, g_dtype="f32"):
     """Elementwise bound on the GPU encode's |T - T_ref| for rows with nterm = psi*ell terms
-    of magnitude sum M = sum_{t,k} |Bc||g|.  fp32 chunk gradients: gamma_n M (one fp32 FMA
-    per term).  bf16 chunk gradients may run on the bf16 matrix cores: each coefficient is
-    split exactly into three bf16 parts, leaving at most u|a| unrepresented, and the 3n
-    products are accumulated in fp32; each accumulation is allowed 2u (the matrix cores'
-    rounding of their internal sums is not assumed to be to nearest): u M + gamma'_{3n+1} M
-    with gamma'_k = 2ku / (1 - 2ku).  That also bounds the vector path."""
+    of magnitude sum M = sum_{t,k} |Bc||g|.  Every path may run on the bf16 matrix cores,
+    where each fp32 coefficient a is split by rounding into three bf16 parts (leaving at most
+    u|a|), the parts' products are exact in fp32 and are accumulated in fp32, each
+    accumulation allowed 2u (the matrix cores' rounding of their internal sums is not assumed
+    to be to nearest): gamma'_k = 2ku / (1 - 2ku).
+    bf16 chunk gradients: three products per term, u M + gamma'_{3n+1} M.
+    fp32 chunk gradients: each g is split exactly into three bf16 parts by truncation
+    (|g2| < 2^-7 |g|, |g3| < 2^-14 |g|) and six of the nine products are kept; the three
+    dropped ones and the coefficient's residue stay below 8u |a||g| per term, and the kept
+    ones sum to at most 1.02 |a||g|: 8u M + 1.02 gamma'_{6n+1} M.  Both also bound the
+    vector path's gamma_n M."""
     return encode_eps(nterm, g_dtype)[..., None] * M
 
 
 def encode_eps(nterm, g_dtype="f32"):
-    """The factor of encode_bound: gamma_n (fp32), u + gamma'_{3n+1} (bf16)."""
+    """The factor of encode_bound: u + gamma'_{3n+1} (bf16), 8u + 1.02 gamma'_{6n+1} (fp32)."""
     nterm = np.asarray(nterm, dtype=np.float64)
-    if g_dtype != "bf16":
-        return gamma(nterm)
-    k = 3 * nterm + 1
-    return U + 2 * k * U / (1.0 - 2 * k * U)
+    if g_dtype == "bf16":
+        k = 3 * nterm + 1
+        return U + 2 * k * U / (1.0 - 2 * k * U)
+    k = 6 * nterm + 1
+    return 8 * U + 1.02 * 2 * k * U / (1.0 - 2 * k * U)
 
 
 def coverage_all(O, psi):

@@ -130,6 +130,11 @@ def test_workspace_sizes():
     assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 1) == 4 * 512 * 2 * 16384
     # general path: one residual per sample row and point
     assert gcx.gc_chunk_grads_workspace_size(50, 512, 16385, 2) == 4 * 2 * 50 * 512
+    # matrix cores (b >= 16 points): split-K partials of Z plus the residuals.  200 (b = 64)
+    # or 400 (b = 256) output tiles of Z; 5 splits fill two whole rounds of 512 resident
+    # blocks (4 or 8 splits would leave a last round 1/8 full)
+    assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 64) == 4 * (5 + 1) * 50 * 512 * 64
+    assert gcx.gc_chunk_grads_workspace_size(50, 512, 16384, 256) == 4 * (5 + 1) * 50 * 512 * 256
     # one fp64 partial per (pattern, 4096-wide piece of a block), none when a block has one piece
     assert gcx.gc_reconstruct_workspace_size(10000, 50, 16384, 1) == 8 * 10000 * 4
     assert gcx.gc_reconstruct_workspace_size(10, 50, 4096, 1) == 0

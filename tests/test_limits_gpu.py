@@ -58,7 +58,7 @@ def test_abi_limits():
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, G.astype(np.float64), ell)
     sent = psi > 0
     assert np.isnan(T[~sent]).all()
-    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= R_.encode_bound(nterm, M, "f32")[sent]).all()
 
     # combine on the oracle's transmitted vectors
     T32 = T_ref.astype(np.float32)

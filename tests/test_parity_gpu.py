@@ -252,7 +252,7 @@ def test_encode_and_reconstruct_edge_patterns():
         T = host(gcx.gc_encode(G_torch(wl, G), dev(psi), dev(order), dev(Bc32), T=Td))
         T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, Gw, ell)
         assert np.isnan(T[~sent]).all()
-        bound = (R_.gamma(nterm)[:, :, None] * M)[sent]
+        bound = R_.encode_bound(nterm, M, wl.g_dtype)[sent]
         assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= bound).all()
         T32 = T_ref.astype(np.float32)  # rows of workers with psi = 0 are zero in the oracle's T
         T32_poison = T32.copy()
@@ -442,7 +442,7 @@ def test_encode_clamps_psi(wl, ell):
     T_ref, M, nterm = R_.encode_ref(Bc.astype(np.float64), clamped, order, OP.widen(G, wl.g_dtype), ell)
     sent = clamped > 0
     assert np.isnan(T[~sent]).all()
-    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= R_.encode_bound(nterm, M, wl.g_dtype)[sent]).all()
 
 
 @pytest.mark.parametrize("ell,d", [(1, 512), (2, 513)])
@@ -461,7 +461,7 @@ def test_encode_many_chunks(ell, d):
     T = host(gcx.gc_encode(dev(G), dev(psi), dev(order), dev(Bc)))
     T_ref, M, nterm = R_.encode_ref(Bc.astype(np.float64), psi, order, G.astype(np.float64), ell)
     sent = psi > 0
-    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    assert (np.abs(T[sent].astype(np.float64) - T_ref[sent]) <= R_.encode_bound(nterm, M, "f32")[sent]).all()
 
 
 def _uneven_assignment(seed=5):
@@ -508,7 +508,7 @@ def test_uneven_non_square_assignment(ell):
     T = host(gcx.gc_encode(dev(G), dev(psi), dev(order), dev(Bc32)))
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), psi, order, G.astype(np.float64), ell)
     sent = psi > 0
-    assert (np.abs(T[sent] - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    assert (np.abs(T[sent] - T_ref[sent]) <= R_.encode_bound(nterm, M, "f32")[sent]).all()
     T32 = T_ref.astype(np.float32)
     gh, _ = gcx.gc_reconstruct(dev(T32), dev(R), d, psi=dev(psi))
     gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, d)

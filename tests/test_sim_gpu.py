@@ -102,7 +102,7 @@ def test_graph_assignment_decode_encode_combine(ell, source):
     T = host(gcx.gc_encode(dev(G), dev(ps), dev(order), dev(Bc32)))
     T_ref, M, nterm = R_.encode_ref(Bc32.astype(np.float64), ps, order, G, ell)
     sent = ps > 0
-    assert (np.abs(T[sent] - T_ref[sent]) <= (R_.gamma(nterm)[:, :, None] * M)[sent]).all()
+    assert (np.abs(T[sent] - T_ref[sent]) <= R_.encode_bound(nterm, M, "f32")[sent]).all()
     T32 = T_ref.astype(np.float32)
     gh, _ = gcx.gc_reconstruct(dev(T32), dev(R), wl.d, psi=dev(ps))
     gh_ref, mag = R_.reconstruct_ref(T32.astype(np.float64), R, wl.d)
