@@ -57,12 +57,11 @@ def parse(argv=None):
                          "and its least-squares run at ell = 1, 2, 4")
     ap.add_argument("--large-batch", type=int, default=0,
                     help="patterns per encode/combine call on the m = 200 workload (0: by ell)")
-    ap.add_argument("--experiment", choices=["hotpath", "completion", "trigger", "ordering", "shapes"],
+    ap.add_argument("--experiment", choices=["hotpath", "completion", "trigger", "ordering"],
                     default="hotpath",
                     help="hotpath: the headline step (default); completion: exact-GC completion times, "
                          "proposed vs original GC; trigger: error vs deadline, proposed vs original GC; "
-                         "ordering: Algorithm 2 vs the best of 100 random orderings; shapes: encode and "
-                         "combine on the m = 100 and m = 200 workloads")
+                         "ordering: Algorithm 2 vs the best of 100 random orderings")
     ap.add_argument("--trials", type=int, default=1000)
     ap.add_argument("--mfma-points", type=int, default=256,
                     help="also time the chunk gradients at this many evaluation points (matrix-core "
@@ -767,76 +766,14 @@ def experiment_ordering(args):
     print(json.dumps(out))
 
 
-def experiment_shapes(args):
-    """Encode and combine on the given-gradient workloads, one batch of patterns per call as
-    their parity tests run them: m = 100, d = 2^20 fp32 (48 patterns, ell = 1, 2, 8) and
-    m = 200, d = 2^24 bf16 (2 patterns of the 50%-straggler run, ell = 1, 2, 4).  One JSON
-    object per (workload, ell): time per call (HIP events, 1 warm-up + 5 calls), bytes of T
-    written / read (transmitting rows only), of G read once, the rates, and the estimates
-    decoded per second by encode + combine (coefficients timed separately: decode_large)."""
-    import torch
-
-    from paper_2405_19509_amd import gcx
-    from workloads import BANDWIDTH, LARGE, gen
-    gcx.load()
-    dev = torch.device("cuda:0")
-
-    def timed(f, reps=5):
-        f()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            f()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / reps
-
-    for wl, batch, ells, variant in ((BANDWIDTH, 48, (1, 2, 8), "exact"), (LARGE, 2, (1, 2, 4), "ls")):
-        G = gen.given_G(wl, threads=16)
-        esize = G.dtype.itemsize
-        if wl.g_dtype == "bf16":
-            Gd = torch.from_numpy(G.view(np.int16)).to(dev).view(torch.bfloat16)
-        else:
-            Gd = torch.from_numpy(G).to(dev)
-        del G
-        psi = gen.psi(wl, count=batch, variant=variant)
-        sent = int((psi > 0).sum())
-        _, order, holder, hpos = gcx.gc_assign(gcx.GC_ASSIGN_CYCLIC, wl.N, wl.m, wl.s)
-        psid, od, hd, hpd = (torch.from_numpy(a).to(dev) for a in (psi, order, holder, hpos))
-        gsum = gcx.gc_sum_chunks(Gd)
-        for ell in ells:
-            Rd = torch.from_numpy(gen.shared_R(wl.m, ell)).to(dev)
-            _, _, _, Bc = gcx.gc_decode_coeffs(psid, od, hd, hpd, Rd)
-            L = -(-wl.d // ell)
-            T = torch.empty(batch, wl.m, L, device=dev)
-            ghat = torch.empty(batch, wl.d, device=dev)
-            sq = torch.empty(batch, dtype=torch.float64, device=dev)
-            ws = torch.empty(max(1, gcx.gc_reconstruct_workspace_size(batch, wl.m, wl.d, ell)),
-                             dtype=torch.uint8, device=dev)
-            te = timed(lambda: gcx.gc_encode(Gd, psid, od, Bc, T=T))
-            tr = timed(lambda: gcx.gc_reconstruct(T, Rd, wl.d, psi=psid, ghat=ghat, gsum=gsum, sqerr=sq,
-                                                  workspace=ws))
-            t_bytes, g_bytes = 4 * sent * L, esize * wl.N * wl.d
-            print(json.dumps({
-                "workload": wl.name, "ell": ell, "patterns_per_call": batch, "transmitting_rows": sent,
-                "terms_per_output": wl.delta * ell,
-                "encode": {"ms": te, "T_GBps": t_bytes / te / 1e6, "T_plus_G_GBps": (t_bytes + g_bytes) / te / 1e6},
-                "combine": {"ms": tr, "GBps": (t_bytes + 4 * batch * wl.d) / tr / 1e6},
-                "decoded_gradients_per_s": batch / ((te + tr) * 1e-3),
-                "T_bytes": t_bytes, "G_bytes": g_bytes}), flush=True)
-            del T, ghat, ws
-            torch.cuda.empty_cache()
-        del Gd
-        torch.cuda.empty_cache()
-
-
 def configs_only(args):
     """One workload's configs (or the 100,000-pattern coefficients) alone, for traces and
     counters per workload; prints their JSON (not the bench line)."""
-    procs = min(CPU_PROCS_MAX, len(os.sched_getaffinity(0)))
+    # patterns generated in this process: under a profiler, forked workers can hang in the
+    # profiler's own teardown
+    from workloads import LARGE, gen
     large = args.configs_only in ("given_m200_d16M_bf16", "decode_large")
-    psi_large = large_patterns(procs) if large else None
+    psi_large = gen.psi(LARGE) if large else None
     import torch
 
     from paper_2405_19509_amd import gcx
@@ -862,8 +799,6 @@ def main():
         return experiment_trigger(args)
     if args.experiment == "ordering":
         return experiment_ordering(args)
-    if args.experiment == "shapes":
-        return experiment_shapes(args)
     if args.configs_only:
         return configs_only(args)
 
