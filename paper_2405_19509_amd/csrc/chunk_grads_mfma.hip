@@ -8,8 +8,9 @@
 // Both run as 128 x 128-tiled GEMMs on v_mfma_f32_32x32x2f32: a 256-thread
 // block holds a 128 x 128 output tile as four 64 x 64 wave tiles (2 x 2 MFMA
 // tiles of 32 x 32 each); operands are staged through double-buffered LDS,
-// 32 values of K per stage, with the next stage's global loads in flight
-// while the current one feeds the MFMAs.  fp32 in, fp32 accumulation.
+// 32 values of K per stage, with the global loads of the stage after next in
+// flight (two register sets) while the current one feeds the MFMAs.  fp32 in,
+// fp32 accumulation.
 //
 //   zw_kernel     Z partials over a split of K = d (split-K keeps >= ~3 waves
 //                 of blocks on 256 CUs); both operands are K-contiguous, held
@@ -23,6 +24,8 @@
 //                 held in LDS as [k][row].
 // Along the points both kernels use 128-wide tiles when b is a multiple of 128 and
 // 64-wide tiles otherwise, so b = 64 does not spend half the MFMAs on padding.
+#include <type_traits>
+
 #include "common.h"
 
 namespace gcx {
@@ -71,23 +74,24 @@ __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restric
   const int64_t k1 = k0 + kper < d ? k0 + kper : d;
   const int lrow = t >> 3, lk = (t & 7) * 4;
 
-  float4 ra[4], rb[4];
-  auto gload = [&](int64_t kb) {
+  // two register sets: the stage after next loads while this stage feeds the MFMAs
+  float4 ra[2][4], rb[2][4];
+  auto gload = [&](int set, int64_t kb) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       const int row = lrow + 32 * p;
       const int64_t k = kb + lk;
       const int r = mt * kTM + row, q = nt * TB + row;
-      ra[p] = (r < n && k < k1) ? ld4(Xi + int64_t(r) * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-      rb[p] = (row < TB && q < b && k < k1) ? ld4(W + int64_t(q) * d + k)
-                                            : make_float4(0.f, 0.f, 0.f, 0.f);
+      ra[set][p] = (r < n && k < k1) ? ld4(Xi + int64_t(r) * d + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+      rb[set][p] = (row < TB && q < b && k < k1) ? ld4(W + int64_t(q) * d + k)
+                                                 : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](int set, int buf) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      *reinterpret_cast<float4 *>(&As[buf][lrow + 32 * p][lk]) = ra[p];
-      if (lrow + 32 * p < TB) *reinterpret_cast<float4 *>(&Bs[buf][lrow + 32 * p][lk]) = rb[p];
+      *reinterpret_cast<float4 *>(&As[buf][lrow + 32 * p][lk]) = ra[set][p];
+      if (lrow + 32 * p < TB) *reinterpret_cast<float4 *>(&Bs[buf][lrow + 32 * p][lk]) = rb[set][p];
     }
   };
 
@@ -100,20 +104,22 @@ __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restric
       for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
 
   const int64_t nst = ceil_div(k1 - k0, kTK);
-  gload(k0);
-  lstore(0);
+  gload(0, k0);
+  if (nst > 1) gload(1, k0 + kTK);
+  lstore(0, 0);
   __syncthreads();
-  for (int64_t st = 0; st < nst; ++st) {
-    const int buf = int(st & 1);
-    if (st + 1 < nst) gload(k0 + (st + 1) * kTK);
+  // stage st is in LDS buffer st & 1, stage st + 1 in register set (st + 1) & 1
+  auto stage = [&](int64_t st, auto setc) {
+    constexpr int SET = decltype(setc)::value;  // st & 1
+    if (st + 2 < nst) gload(SET, k0 + (st + 2) * kTK);
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
       float4 a[2], bb[NB];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) a[mb] = ld4(&As[buf][wm * 64 + mb * 32 + li][h * 16 + s4 * 4]);
+      for (int mb = 0; mb < 2; ++mb) a[mb] = ld4(&As[SET][wm * 64 + mb * 32 + li][h * 16 + s4 * 4]);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        bb[nb] = ld4(&Bs[buf][wn * (TB / 2) + nb * 32 + li][h * 16 + s4 * 4]);
+        bb[nb] = ld4(&Bs[SET][wn * (TB / 2) + nb * 32 + li][h * 16 + s4 * 4]);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -122,8 +128,12 @@ __global__ __launch_bounds__(kMThreads, 2) void zw_kernel(const float *__restric
           for (int nb = 0; nb < NB; ++nb)
             acc[mb][nb] = mfma32(comp(a[mb], e), comp(bb[nb], e), acc[mb][nb]);
     }
-    if (st + 1 < nst) lstore(buf ^ 1);
+    if (st + 1 < nst) lstore(SET ^ 1, SET ^ 1);
     __syncthreads();
+  };
+  for (int64_t st = 0; st < nst; st += 2) {
+    stage(st, std::integral_constant<int, 0>{});
+    if (st + 1 < nst) stage(st + 1, std::integral_constant<int, 1>{});
   }
 
   float *Zs = Zp + (int64_t(s) * N + i) * int64_t(n) * b;
@@ -170,23 +180,24 @@ __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restri
   const float *Uc = Ui + i * int64_t(n) * b;
   const int lrow = t >> 5, lc = (t & 31) * 4;
 
-  float4 ra[4], rb[4];
-  auto gload = [&](int kb) {
+  // two register sets: the stage after next loads while this stage feeds the MFMAs
+  float4 ra[2][4], rb[2][4];
+  auto gload = [&](int set, int kb) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       const int r = kb + lrow + 8 * p;
       const int q = mt * TB + lc;
       const int64_t x = nt * kTN + lc;
-      ra[p] = (lc < TB && r < n && q < b) ? ld4(Uc + int64_t(r) * b + q)
-                                          : make_float4(0.f, 0.f, 0.f, 0.f);
-      rb[p] = (r < n && x < d) ? ld4(Xi + int64_t(r) * d + x) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ra[set][p] = (lc < TB && r < n && q < b) ? ld4(Uc + int64_t(r) * b + q)
+                                               : make_float4(0.f, 0.f, 0.f, 0.f);
+      rb[set][p] = (r < n && x < d) ? ld4(Xi + int64_t(r) * d + x) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](int set, int buf) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      if (lc < TB) *reinterpret_cast<float4 *>(&As[buf][lrow + 8 * p][lc]) = ra[p];
-      *reinterpret_cast<float4 *>(&Bs[buf][lrow + 8 * p][lc]) = rb[p];
+      if (lc < TB) *reinterpret_cast<float4 *>(&As[buf][lrow + 8 * p][lc]) = ra[set][p];
+      *reinterpret_cast<float4 *>(&Bs[buf][lrow + 8 * p][lc]) = rb[set][p];
     }
   };
 
@@ -199,26 +210,32 @@ __global__ __launch_bounds__(kMThreads, 2) void utx_kernel(const float *__restri
       for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
 
   const int nst = int(ceil_div(n, kTK));
-  gload(0);
-  lstore(0);
+  gload(0, 0);
+  if (nst > 1) gload(1, kTK);
+  lstore(0, 0);
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nst) gload((st + 1) * kTK);
+  // stage st is in LDS buffer st & 1, stage st + 1 in register set (st + 1) & 1
+  auto stage = [&](int st, auto setc) {
+    constexpr int SET = decltype(setc)::value;  // st & 1
+    if (st + 2 < nst) gload(SET, (st + 2) * kTK);
 #pragma unroll
     for (int s = 0; s < kTK / 2; ++s) {
       float a[MB], bb[2];
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) a[mb] = As[buf][2 * s + h][wm * (TB / 2) + mb * 32 + li];
+      for (int mb = 0; mb < MB; ++mb) a[mb] = As[SET][2 * s + h][wm * (TB / 2) + mb * 32 + li];
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) bb[nb] = Bs[buf][2 * s + h][wn * 64 + nb * 32 + li];
+      for (int nb = 0; nb < 2; ++nb) bb[nb] = Bs[SET][2 * s + h][wn * 64 + nb * 32 + li];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = mfma32(a[mb], bb[nb], acc[mb][nb]);
     }
-    if (st + 1 < nst) lstore(buf ^ 1);
+    if (st + 1 < nst) lstore(SET ^ 1, SET ^ 1);
     __syncthreads();
+  };
+  for (int st = 0; st < nst; st += 2) {
+    stage(st, std::integral_constant<int, 0>{});
+    if (st + 1 < nst) stage(st + 1, std::integral_constant<int, 1>{});
   }
 
 #pragma unroll

@@ -683,10 +683,12 @@ __device__ __forceinline__ void decode_cyclic_l1(const int32_t *__restrict__ psi
       const double *fr = F + j4 + t4;
       const int lim = pss[j4 + delta] - t4;  // positions t4 + q with q < lim are processed
       const double r = Rs[j4];
-      float o[4];
+      // every F entry read here is set, so the four reads are unconditional (paired LDS
+      // reads) and the prefix is applied as a bit mask
+      uint32_t o[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = q < lim ? float(r * fr[q]) : 0.f;
-      *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
+      for (int q = 0; q < 4; ++q) o[q] = __float_as_uint(float(r * fr[q])) & (q < lim ? ~0u : 0u);
+      *reinterpret_cast<uint4 *>(Bp + e0) = make_uint4(o[0], o[1], o[2], o[3]);
       j4 += j4_step;
       t4 += t4_step;
       if (t4 >= delta) {
@@ -698,7 +700,8 @@ __device__ __forceinline__ void decode_cyclic_l1(const int32_t *__restrict__ psi
     int j = lane / delta, t = lane % delta;
     const int j_step = kWave / delta, t_step = kWave % delta;
     for (int e = lane; e < nrow; e += kWave) {
-      Bp[e] = pss[j + delta] > t ? float(double(Rs[j]) * F[j + t]) : 0.f;
+      const uint32_t v = __float_as_uint(float(double(Rs[j]) * F[j + t]));
+      Bp[e] = __uint_as_float(v & (pss[j + delta] > t ? ~0u : 0u));
       j += j_step;
       t += t_step;
       if (t >= delta) {
