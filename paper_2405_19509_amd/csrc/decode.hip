@@ -24,6 +24,16 @@ namespace {
 constexpr int kDecodeThreads = 256;
 constexpr int kDecodeWaves = kDecodeThreads / kWave;
 
+// Coefficients are written once and read only by later calls: non-temporal stores (measured
+// 15% faster for the 1.6 GB of coefficients of 100,000 patterns at m = 200, delta = 20 than
+// plain ones).  Coverage rows (4N bytes per pattern, not whole cache lines) stay plain:
+// non-temporal stores of them measured slower.
+__device__ __forceinline__ void st_nt(float *p, float v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ void st_nt4(float *p, float a, float b, float c, float d) {
+  typedef float v4f_ __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(v4f_{a, b, c, d}, reinterpret_cast<v4f_ *>(p));
+}
+
 // One pattern by one wavefront, one lane per chunk: coverage, decodability, coefficient
 // error and the chunk's coefficients written straight to their (worker, position) slots.
 template <int ELL>
@@ -48,7 +58,7 @@ __device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int6
         ++load;
       } else if (want_bc) {
 #pragma unroll
-        for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
+        for (int k = 0; k < ELL; ++k) st_nt(Bp + j * wstride + t * ELL + k, 0.f);
       }
     }
     const int v = ps[j];
@@ -77,7 +87,7 @@ __device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int6
         const int j = hi[u], t = hp[u];
         if (j >= 0 && j < m && t >= 0 && t < delta) {
 #pragma unroll
-          for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
+          for (int k = 0; k < ELL; ++k) st_nt(Bp + j * wstride + t * ELL + k, 0.f);
         }
       }
       continue;
@@ -95,7 +105,7 @@ __device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int6
       for (int u = 0; u < gamma; ++u) {
         const int j = hi[u], t = hp[u];
         if (j >= 0 && j < m && t >= 0 && t < delta)
-          Bp[j * wstride + t] = ps[j] > t ? float(double(Rs[j]) / ss) : 0.f;
+          st_nt(Bp + j * wstride + t, ps[j] > t ? float(double(Rs[j]) / ss) : 0.f);
       }
     } else if (Delta >= ELL) {
       // M = X X^T, lower triangle
@@ -127,10 +137,10 @@ __device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int6
           for (int k = 0; k < ELL; ++k) c[k] = Rs[k * m + j];
           chol_solve<ELL>(M, c);
 #pragma unroll
-          for (int k = 0; k < ELL; ++k) dst[k] = float(c[k]);
+          for (int k = 0; k < ELL; ++k) st_nt(dst + k, float(c[k]));
         } else {
 #pragma unroll
-          for (int k = 0; k < ELL; ++k) dst[k] = 0.f;
+          for (int k = 0; k < ELL; ++k) st_nt(dst + k, 0.f);
         }
       }
     } else {
@@ -152,7 +162,7 @@ __device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int6
           ++cnt;
         } else {
 #pragma unroll
-          for (int k = 0; k < ELL; ++k) Bp[j * wstride + t * ELL + k] = 0.f;
+          for (int k = 0; k < ELL; ++k) st_nt(Bp + j * wstride + t * ELL + k, 0.f);
         }
       }
       double X[ELL][ELL];  // X[k][a] = R[k][selj[a]], zero for a >= Delta
@@ -186,7 +196,7 @@ __device__ __forceinline__ void decode_one(const int32_t *__restrict__ psi, int6
           double c = 0.0;
 #pragma unroll
           for (int b = 0; b < ELL; ++b) c += z[b] * X[k][b];
-          dst[k] = float(c);
+          st_nt(dst + k, float(c));
         }
       }
     }
@@ -468,7 +478,7 @@ __attribute__((amdgpu_waves_per_eu(ELL <= 2 ? 8 : 1))) void decode_tiled_kernel(
           const float v = float(r * f[q]);
           o[q] = (pv > t4 + q && f[q] != 0.0) ? v : 0.f;
         }
-        *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
+        st_nt4(Bp + e0, o[0], o[1], o[2], o[3]);
         j4 += j4_step;
         t4 += t4_step;
         if (t4 >= delta) {
@@ -506,7 +516,7 @@ __attribute__((amdgpu_waves_per_eu(ELL <= 2 ? 8 : 1))) void decode_tiled_kernel(
           const float v = float(double(r[q]) * f[q]);
           o[q] = (pv[q] > tq[q] && f[q] != 0.0) ? v : 0.f;
         }
-        *reinterpret_cast<float4 *>(Bp + e0) = make_float4(o[0], o[1], o[2], o[3]);
+        st_nt4(Bp + e0, o[0], o[1], o[2], o[3]);
         j4 += j4_step;
         t4 += t4_step;
         if (t4 >= delta) {
@@ -576,7 +586,7 @@ __attribute__((amdgpu_waves_per_eu(ELL <= 2 ? 8 : 1))) void decode_tiled_kernel(
           }
         }
   #pragma unroll
-        for (int k = 0; k < ELL; ++k) Bp[int64_t(e) * ELL + k] = out[k];
+        for (int k = 0; k < ELL; ++k) st_nt(Bp + int64_t(e) * ELL + k, out[k]);
         j += j_step;
         t += t_step;
         if (t >= delta) {
@@ -675,7 +685,7 @@ __device__ __forceinline__ void decode_cyclic_l1(const int32_t *__restrict__ psi
   float *Bp = Bc + p * int64_t(m) * delta;
   const int nrow = m * delta;
   if (invalid) {
-    for (int e = lane; e < nrow; e += kWave) Bp[e] = 0.f;
+    for (int e = lane; e < nrow; e += kWave) st_nt(Bp + e, 0.f);
   } else if ((delta & 3) == 0 && (reinterpret_cast<uintptr_t>(Bp) & 15) == 0) {
     int j4 = (4 * lane) / delta, t4 = (4 * lane) % delta;
     const int j4_step = (4 * kWave) / delta, t4_step = (4 * kWave) % delta;
@@ -688,7 +698,7 @@ __device__ __forceinline__ void decode_cyclic_l1(const int32_t *__restrict__ psi
       uint32_t o[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) o[q] = __float_as_uint(float(r * fr[q])) & (q < lim ? ~0u : 0u);
-      *reinterpret_cast<uint4 *>(Bp + e0) = make_uint4(o[0], o[1], o[2], o[3]);
+      st_nt4(Bp + e0, __uint_as_float(o[0]), __uint_as_float(o[1]), __uint_as_float(o[2]), __uint_as_float(o[3]));
       j4 += j4_step;
       t4 += t4_step;
       if (t4 >= delta) {
@@ -701,7 +711,7 @@ __device__ __forceinline__ void decode_cyclic_l1(const int32_t *__restrict__ psi
     const int j_step = kWave / delta, t_step = kWave % delta;
     for (int e = lane; e < nrow; e += kWave) {
       const uint32_t v = __float_as_uint(float(double(Rs[j]) * F[j + t]));
-      Bp[e] = __uint_as_float(v & (pss[j + delta] > t ? ~0u : 0u));
+      st_nt(Bp + e, __uint_as_float(v & (pss[j + delta] > t ? ~0u : 0u)));
       j += j_step;
       t += t_step;
       if (t >= delta) {
