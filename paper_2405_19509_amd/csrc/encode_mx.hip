@@ -17,15 +17,20 @@
 // v_mfma_f32_32x32x16_bf16 accumulates them in fp32.
 //
 // Layout: a block owns a group of J consecutive workers, a window of PB patterns
-// (J * PB = 64 candidate rows (pattern, worker), candidate r = pb * J + jb) and a range of
-// slices of x walked in turn.  The window's transmitting rows (psi > 0) are compacted into
-// one or two 32-row tiles (stragglers cost nothing), whose coefficients, split into three
-// bf16 planes, are built once per block.  Per slice the block stages the slices of the
-// group's union of chunks (J + delta - 1 chunks under the cyclic order), one row per (slot,
-// block), and every row tile is computed against them:
+// (J * PB = 64 or 128 candidate rows (pattern, worker), candidate r = pb * J + jb) and a
+// range of slices of x walked in turn.  The window's transmitting rows (psi > 0) are
+// compacted into full 32-row tiles (stragglers cost nothing), whose coefficients, split
+// into three bf16 planes, are built once per block.  Per slice the block stages the slices
+// of the group's union of chunks (J + delta - 1 chunks under the cyclic order), one row per
+// (slot, block), and every row tile is computed against them:
 //   bf16: 512-wide slices staged straight from memory to LDS (1 KB rows); each of the 8
 //         waves takes two 32 x 32 output tiles per row tile, per 16-deep K step three bf16x8
-//         coefficient loads, eight 16-bit gathers of the staged column per tile, six MFMAs;
+//         coefficient loads, eight 16-bit gathers of the staged column per tile, six MFMAs.
+//         Where the group's rows need 3+ K steps, 128-candidate windows with 256-wide
+//         slices: the union of twice the workers is not much larger, so the rows staged per
+//         row written nearly halve; each wave takes one 32-wide column, gathered once per K
+//         step for all (up to four) row tiles.  From 4 K steps on a block fills a CU's LDS
+//         and the K loop is unrolled into the registers that frees;
 //   fp32: 256-wide slices staged through registers with the staged rows fastest, so that a
 //         lane's eight K values of one position are two 16-byte reads, split once per slice
 //         for both row tiles; each wave takes one 32-position tile, six MFMAs per row tile
@@ -50,6 +55,9 @@ constexpr int kMxRowBytes = kMxW * 2 + 16;   // staged row stride: padded so row
 constexpr int kMxfMaxWideKS = 3;             // fp32: 512-wide slices (1024 threads) up to 3 K steps
 static_assert(kMxW == (kMxThreads / 64) * 64 && kMxW * 2 == 64 * 16, "bf16: two 32-wide tiles per wave, 16 bytes per lane and staged row");
 constexpr int kMxMaxKS = 6;                  // K steps of 16 (at most 96 staged rows)
+// bf16: 128-candidate windows (256-wide slices, one tile per wave) where a 64-candidate
+// window would need this many K steps
+constexpr int kMxWinKS = 3;
 constexpr size_t kMxLds = 152 * 1024;
 
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
@@ -111,30 +119,38 @@ struct MxArgs {
 };
 
 // Slice region of the LDS, by chunk-gradient type:
-//   bf16: Kp staged rows x kMxRowBytes, position fastest (filled straight from memory)
+//   bf16: Kp staged rows x RB bytes, position fastest (filled straight from memory)
 //   fp32: W positions x (Kp + 4) floats, staged row fastest (a lane's eight K values of
 //         one position are two 16-byte reads)
-template <typename GT, int KS>
+template <typename GT, int KS, int CW>
 struct MxLayout {
   static constexpr bool F32 = sizeof(GT) == 4;
   static constexpr int Kp = 16 * KS;
+  static_assert(CW == 64 || (CW == 128 && !F32), "64 candidates, or 128 with bf16 chunk gradients");
+  static constexpr bool WIN = CW == 128;  // 256-wide slices, one 32-wide tile per wave
+  static constexpr int NT = CW / 32;      // row tiles at most
   // fp32: one 32-wide tile per wave, 2 KB row segments of T per slice (16 waves) while the
   // staged rows fit, else 256 positions (8 waves); bf16: two tiles per wave, 512 positions
   static constexpr int THREADS = F32 && KS <= kMxfMaxWideKS ? 1024 : kMxThreads;
   static constexpr int WAVES = THREADS / 64;
-  static constexpr int W = F32 ? 32 * WAVES : kMxW;  // positions per slice
+  static constexpr int W = F32 || WIN ? 32 * WAVES : kMxW;  // positions per slice
+  static constexpr int RB = W * 2 + 16;              // bf16: staged row stride in bytes
   static constexpr int BS = Kp + 4;                  // fp32: floats per staged position
-  static constexpr size_t slice_bytes = F32 ? size_t(W) * BS * 4 : size_t(Kp) * kMxRowBytes;
+  static constexpr size_t slice_bytes = F32 ? size_t(W) * BS * 4 : size_t(Kp) * RB;
+  // bf16 from 4 K steps on the staged rows allow one block per CU: registers for the K loop
+  // unrolled, so the LDS reads of one step overlap the products of the previous one
+  static constexpr int WPE = !F32 && KS >= 4 ? 2 : 4;
+  static constexpr int UNR = !F32 && KS >= 4 ? KS : 1;
   static_assert(!F32 || (W / 2) % 128 == 0, "fp32 staging: two positions per thread, whole waves per row group");
 };
 
-// LDS: [ slice region ][ Ap: 2 tiles x 3 planes x 32 rows x AP bf16 ]
+// LDS: [ slice region ][ Ap: CW/32 tiles x 3 planes x 32 rows x AP bf16 ]
 //      [ rdesc: 2 int64 per row ][ map: N int32 ][ slotc: slots int32 ][ code: J*delta int32 ]
 // The coefficient rows are first assembled in fp32 over the slice region, then split into Ap.
-template <typename GT, int KS>
-__global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_waves_per_eu(4))) void encode_mx_kernel(
+template <typename GT, int KS, int CW>
+__global__ __launch_bounds__((MxLayout<GT, KS, CW>::THREADS)) __attribute__((amdgpu_waves_per_eu(MxLayout<GT, KS, CW>::WPE))) void encode_mx_kernel(
     MxArgs a) {
-  using Lay = MxLayout<GT, KS>;
+  using Lay = MxLayout<GT, KS, CW>;
   constexpr int NTH = Lay::THREADS;
   constexpr bool F32 = Lay::F32;
   constexpr int Kp = Lay::Kp;
@@ -142,16 +158,17 @@ __global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_
   extern __shared__ __align__(16) unsigned char lds[];
   unsigned char *Gs = lds;
   uint16_t *Ap = reinterpret_cast<uint16_t *>(lds + Lay::slice_bytes);
-  int64_t *rdesc = reinterpret_cast<int64_t *>(Ap + 2 * 3 * 32 * AP);
+  int64_t *rdesc = reinterpret_cast<int64_t *>(Ap + Lay::NT * 3 * 32 * AP);
   int32_t *map = reinterpret_cast<int32_t *>(rdesc + 2 * Kp);
   int32_t *slotc = map + a.N;
   int32_t *code = slotc + a.slots;
-  float *Af = reinterpret_cast<float *>(Gs);  // [64][Kp] fp32, before the slices are staged
+  float *Af = reinterpret_cast<float *>(Gs);  // [CW][Kp] fp32, before the slices are staged
+  static_assert(size_t(CW) * Kp * 4 <= Lay::slice_bytes, "coefficient rows fit the slice region");
   __shared__ int nslot_s, nuni_s, nsend_s;
-  __shared__ int8_t ccomp_s[64];    // compacted row of each candidate, or -1
+  __shared__ int8_t ccomp_s[CW];    // compacted row of each candidate, or -1
   // each compacted row's element offset in T from the window's first row (pattern p0,
   // worker j0): (pb * m + jb) * L; read two at a time by the stores
-  __shared__ __align__(16) int64_t rowoff_s[64];
+  __shared__ __align__(16) int64_t rowoff_s[CW];
 
   // block -> (slice range, unit = (group, pattern tile)); XCD x takes ranges x, x + 8, ...
   const int64_t b = blockIdx.x;
@@ -232,22 +249,26 @@ __global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_
     }
     // the transmitting candidates of the pass, compacted in candidate order
     if (tid < kWave) {
-      const int r = tid, pb = r / a.J, jb = r % a.J;
-      const int64_t p = p0 + pb;
-      const bool on = pb < a.PB && p < a.P && jb >= ja && jb < jn && a.psi[p * a.m + j0 + jb] > 0;
-      const unsigned long long mk = __ballot(on);
-      const int c = __popcll(mk & ((1ull << r) - 1));
-      ccomp_s[r] = on ? int8_t(c) : int8_t(-1);
-      if (on) rowoff_s[c] = (int64_t(pb) * a.m + jb) * a.L;
-      if (tid == 0) nsend_s = __popcll(mk);
+      int cnt = 0;
+      for (int r0 = 0; r0 < CW; r0 += kWave) {
+        const int r = r0 + tid, pb = r / a.J, jb = r % a.J;
+        const int64_t p = p0 + pb;
+        const bool on = pb < a.PB && p < a.P && jb >= ja && jb < jn && a.psi[p * a.m + j0 + jb] > 0;
+        const unsigned long long mk = __ballot(on);
+        const int c = cnt + __popcll(mk & ((1ull << tid) - 1));
+        ccomp_s[r] = on ? int8_t(c) : int8_t(-1);
+        if (on) rowoff_s[c] = (int64_t(pb) * a.m + jb) * a.L;
+        cnt += __popcll(mk);
+      }
+      if (tid == 0) nsend_s = cnt;
     }
-    for (int e = tid; e < 64 * Kp; e += NTH) Af[e] = 0.f;
+    for (int e = tid; e < CW * Kp; e += NTH) Af[e] = 0.f;
     __syncthreads();
     const int nsend = nsend_s;
     const int ntile = (nsend + 31) / 32;
     // compacted row c (candidate (pattern p0 + r / J, worker j0 + r % J)), column s*ell + k:
     // zero past the row's processed prefix
-    for (int e = tid; e < 64 * a.delta; e += NTH) {
+    for (int e = tid; e < CW * a.delta; e += NTH) {
       const int r = e / a.delta, t = e % a.delta;
       const int c = ccomp_s[r];
       if (c < 0) continue;
@@ -290,8 +311,8 @@ __global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_
     // bf16: rows K .. Kp of the slice region stay zero for the whole pass (fp32: the
     // staging writes them)
     if constexpr (!F32)
-      for (int e = tid; e < (Kp - K) * (kMxRowBytes / 16); e += NTH)
-        reinterpret_cast<uint4 *>(Gs + size_t(K) * kMxRowBytes)[e] = make_uint4(0u, 0u, 0u, 0u);
+      for (int e = tid; e < (Kp - K) * (Lay::RB / 16); e += NTH)
+        reinterpret_cast<uint4 *>(Gs + size_t(K) * Lay::RB)[e] = make_uint4(0u, 0u, 0u, 0u);
     if (ntile == 0) continue;  // nothing transmitted in this window: no slice to stage
 
     for (int64_t slice = s_begin; slice < s_end; ++slice) {
@@ -331,15 +352,15 @@ __global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_
           *reinterpret_cast<float4 *>(d1 + 4) = make_float4(v1[4], v1[5], v1[6], v1[7]);
         }
       } else {
-        // stage: staged row `row` <- 512 positions of its block from x0 (zero past L or d),
+        // stage: staged row `row` <- W positions of its block from x0 (zero past L or d),
         // straight from memory to LDS: one wave instruction per row, lane i filling bytes
-        // 16i .. 16i + 15 of its 1 KB
+        // 16i .. 16i + 15 (256-wide slices: lanes 0 .. 31)
         const uint16_t *Gh = static_cast<const uint16_t *>(a.G);
-        for (int row = wave; row < K; row += Lay::WAVES) {
+        for (int row = wave; row < K && (!Lay::WIN || lane < 32); row += Lay::WAVES) {
           const int64_t base = rdesc[2 * row], lim = rdesc[2 * row + 1];
           const int64_t x = x0 + 8 * lane;
-          unsigned char *dst = Gs + size_t(row) * kMxRowBytes;
-          if (a.stage16 && x0 + kMxW <= lim) {
+          unsigned char *dst = Gs + size_t(row) * Lay::RB;
+          if (a.stage16 && x0 + Lay::W <= lim) {
             __builtin_amdgcn_global_load_lds(Gh + base + x, dst, 16, 0, 0);
           } else {
             uint32_t w[4];
@@ -409,14 +430,67 @@ __global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_
           tiles(std::integral_constant<int, 2>{});
         else
           tiles(std::integral_constant<int, 1>{});
+      } else if constexpr (Lay::WIN) {
+        // one 32-position tile per wave (x0 + 32 wave + li), every row tile in one K loop so
+        // that each gathered column feeds all of them
+        const uint16_t *Gc = reinterpret_cast<const uint16_t *>(Gs) + 32 * wave + li;
+        constexpr int GR = Lay::RB / 2;  // staged row stride in bf16
+        auto tiles = [&](auto ntc) {
+          constexpr int NT = decltype(ntc)::value;
+          v16f acc[NT];
+#pragma unroll
+          for (int t = 0; t < NT; ++t) acc[t] = v16f{};
+#pragma unroll Lay::UNR
+          for (int q = 0; q < KS; ++q) {
+            const int kb = 16 * q + 8 * h;
+            v8bf bq;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) bq[i] = __builtin_bit_cast(__bf16, Gc[(kb + i) * GR]);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+              const uint16_t *At = Ap + t * 3 * 32 * AP;
+              const v8bf a1 = *reinterpret_cast<const v8bf *>(At + (0 * 32 + li) * AP + kb);
+              const v8bf a2 = *reinterpret_cast<const v8bf *>(At + (1 * 32 + li) * AP + kb);
+              const v8bf a3 = *reinterpret_cast<const v8bf *>(At + (2 * 32 + li) * AP + kb);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3, bq, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, bq, acc[t], 0, 0, 0);
+              acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bq, acc[t], 0, 0, 0);
+            }
+          }
+          const int64_t xa = x0 + 32 * wave + li;
+          if (xa >= a.L) return;
+          // lane (h, li) holds D[8(v/4) + 4h + v%4][li]: rows 32t + 8g + 4h + i, their
+          // offsets read four at a time (two 16-byte reads)
+          float *Tx = Tw + xa;
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int cb = 32 * t + 8 * g + 4 * h;
+              const longlong2 o0 = *reinterpret_cast<const longlong2 *>(rowoff_s + cb);
+              const longlong2 o1 = *reinterpret_cast<const longlong2 *>(rowoff_s + cb + 2);
+              const int64_t off[4] = {o0.x, o0.y, o1.x, o1.y};
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                if (cb + i < nsend) __builtin_nontemporal_store(acc[t][4 * g + i], Tx + off[i]);
+            }
+        };
+        if (ntile == 1)
+          tiles(std::integral_constant<int, 1>{});
+        else if (ntile == 2)
+          tiles(std::integral_constant<int, 2>{});
+        else if (ntile == 3)
+          tiles(std::integral_constant<int, 3>{});
+        else
+          tiles(std::integral_constant<int, Lay::NT>{});
       } else {
         // per row tile, two 32 x 32 tiles per wave: positions x0 + 64 wave + 32 c + li
         const uint16_t *Gc = reinterpret_cast<const uint16_t *>(Gs) + 64 * wave + li;
-        constexpr int GR = kMxRowBytes / 2;  // staged row stride in bf16
+        constexpr int GR = Lay::RB / 2;  // staged row stride in bf16
         for (int rt = 0; rt < ntile; ++rt) {
           const uint16_t *At = Ap + rt * 3 * 32 * AP;
           v16f acc0 = {}, acc1 = {};
-#pragma unroll 1
+#pragma unroll Lay::UNR
           for (int q = 0; q < KS; ++q) {
             const int kb = 16 * q + 8 * h;
             const v8bf a1 = *reinterpret_cast<const v8bf *>(At + (0 * 32 + li) * AP + kb);
@@ -458,27 +532,31 @@ __global__ __launch_bounds__((MxLayout<GT, KS>::THREADS)) __attribute__((amdgpu_
   }
 }
 
-template <typename GT, int KS>
+template <typename GT, int KS, int CW>
 int launch_mx_ks(const MxArgs &m, size_t lds, hipStream_t st) {
-  const int64_t blocks = m.nsr * m.ngroups * m.ntp;
-  constexpr int NTH = MxLayout<GT, KS>::THREADS;
-  if (!grid_ok(blocks, NTH)) return GC_EINVAL;
-  if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_mx_kernel<GT, KS>),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
-    return GC_ELAUNCH;
-  hipLaunchKernelGGL((encode_mx_kernel<GT, KS>), dim3(unsigned(blocks)), dim3(NTH), lds, st, m);
-  return GC_OK;
+  if constexpr (CW == 128 && KS < kMxWinKS) {
+    return kEncodeMxNotApplicable;  // never planned: a 128-candidate window has as many K steps
+  } else {                          // as a 64-candidate one, or more
+    const int64_t blocks = m.nsr * m.ngroups * m.ntp;
+    constexpr int NTH = MxLayout<GT, KS, CW>::THREADS;
+    if (!grid_ok(blocks, NTH)) return GC_EINVAL;
+    if (hipFuncSetAttribute(reinterpret_cast<const void *>(&encode_mx_kernel<GT, KS, CW>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess)
+      return GC_ELAUNCH;
+    hipLaunchKernelGGL((encode_mx_kernel<GT, KS, CW>), dim3(unsigned(blocks)), dim3(NTH), lds, st, m);
+    return GC_OK;
+  }
 }
 
-template <typename GT>
+template <typename GT, int CW>
 int launch_mx(const MxArgs &a, int KS, size_t lds, hipStream_t st) {
   switch (KS) {
-    case 1: return launch_mx_ks<GT, 1>(a, lds, st);
-    case 2: return launch_mx_ks<GT, 2>(a, lds, st);
-    case 3: return launch_mx_ks<GT, 3>(a, lds, st);
-    case 4: return launch_mx_ks<GT, 4>(a, lds, st);
-    case 5: return launch_mx_ks<GT, 5>(a, lds, st);
-    case 6: return launch_mx_ks<GT, 6>(a, lds, st);
+    case 1: return launch_mx_ks<GT, 1, CW>(a, lds, st);
+    case 2: return launch_mx_ks<GT, 2, CW>(a, lds, st);
+    case 3: return launch_mx_ks<GT, 3, CW>(a, lds, st);
+    case 4: return launch_mx_ks<GT, 4, CW>(a, lds, st);
+    case 5: return launch_mx_ks<GT, 5, CW>(a, lds, st);
+    case 6: return launch_mx_ks<GT, 6, CW>(a, lds, st);
     default: return kEncodeMxNotApplicable;
   }
 }
@@ -502,11 +580,6 @@ int encode_mx(const void *G, bool f32, int32_t N, int64_t d, const int32_t *psi,
   a.T = T;
   const uintptr_t ga = reinterpret_cast<uintptr_t>(G);
   a.stage16 = f32 ? (d % 2 == 0 && a.L % 2 == 0 && (ga & 7) == 0) : (d % 8 == 0 && a.L % 8 == 0 && (ga & 15) == 0);
-  // up to 64 candidate rows: PB patterns (a power of two covering the call, at most 64) x J
-  // workers, J halved while the group's cyclic union would need more than kMxMaxKS K steps
-  int pb = 1;
-  while (pb < 64 && pb < P) pb *= 2;
-  a.PB = pb;
   // slots for the cyclic union of a group; a block whose union is larger walks its workers
   // one at a time, each needing delta slots
   auto union_slots = [&](int64_t J) {
@@ -514,23 +587,48 @@ int encode_mx(const void *G, bool f32, int32_t N, int64_t d, const int32_t *psi,
     if (sl > N) sl = N;
     return sl < delta ? int64_t(delta) : sl;
   };
-  int64_t J = 64 / pb;
-  if (J > m) J = m;
-  while (J > 1 && ceil_div(union_slots(J) * ell, 16) > kMxMaxKS) J /= 2;
-  a.J = int(J);
+  // a window of cw candidate rows: PB patterns (a power of two covering the call, at most
+  // cw) x J workers, J halved while the group's cyclic union would need more than kMxMaxKS
+  // K steps
+  struct Plan {
+    int pb, J, KS, W;
+    int64_t slots;
+    size_t lds;
+  };
+  auto plan = [&](int cw, Plan &q) {
+    q.pb = 1;
+    while (q.pb < cw && q.pb < P) q.pb *= 2;
+    int64_t J = cw / q.pb;
+    if (J > m) J = m;
+    while (J > 1 && ceil_div(union_slots(J) * ell, 16) > kMxMaxKS) J /= 2;
+    q.J = int(J);
+    q.slots = union_slots(J);
+    const int64_t KS = ceil_div(q.slots * ell, 16);
+    if (KS > kMxMaxKS) return false;
+    q.KS = int(KS);
+    const int Kp = 16 * q.KS;
+    q.W = f32 ? (q.KS <= kMxfMaxWideKS ? 512 : 256) : (cw == 128 ? 256 : kMxW);
+    const size_t slice = f32 ? size_t(q.W) * (Kp + 4) * sizeof(float) : size_t(Kp) * (q.W * 2 + 16);
+    q.lds = slice + sizeof(uint16_t) * (cw / 32) * 3 * 32 * (Kp + 8) + 2 * sizeof(int64_t) * size_t(Kp) +
+            sizeof(int32_t) * (size_t(N) + q.slots + size_t(q.J) * delta);
+    return q.lds <= kMxLds;
+  };
+  Plan q{}, q2{};
+  const bool ok64 = plan(64, q);
+  // bf16: 128-candidate windows, which stage the group's chunks once for up to twice the
+  // rows, where a 64-candidate window would need kMxWinKS or more K steps and the larger
+  // window holds more candidates
+  const bool win = !f32 && (!ok64 || q.KS >= kMxWinKS) && plan(128, q2) &&
+                   (!ok64 || int64_t(q2.pb) * q2.J > int64_t(q.pb) * q.J);
+  if (win) q = q2;
+  else if (!ok64) return kEncodeMxNotApplicable;
+  a.PB = q.pb;
+  a.J = q.J;
   a.ngroups = int(ceil_div(m, a.J));
-  a.ntp = ceil_div(P, pb);
-  const int64_t slots = union_slots(J);
-  a.slots = int(slots);
-  const int64_t K = slots * ell;
-  const int KS = int(ceil_div(K, 16));
-  if (KS > kMxMaxKS) return kEncodeMxNotApplicable;
-  const int Kp = 16 * KS;
-  const int W = f32 ? (KS <= kMxfMaxWideKS ? 512 : 256) : kMxW;
-  const size_t slice = f32 ? size_t(W) * (Kp + 4) * sizeof(float) : size_t(Kp) * kMxRowBytes;
-  const size_t lds = slice + sizeof(uint16_t) * 2 * 3 * 32 * (Kp + 8) + 2 * sizeof(int64_t) * size_t(Kp) +
-                     sizeof(int32_t) * (size_t(N) + slots + size_t(a.J) * delta);
-  if (lds > kMxLds) return kEncodeMxNotApplicable;
+  a.ntp = ceil_div(P, q.pb);
+  a.slots = int(q.slots);
+  const int KS = q.KS, W = q.W;
+  const size_t lds = q.lds;
   a.nslices = int(ceil_div(a.L, W));
   // slice ranges: a multiple of 8 (one share per XCD), about 16 blocks per CU in all
   const int64_t units = int64_t(a.ngroups) * a.ntp;
@@ -539,7 +637,8 @@ int encode_mx(const void *G, bool f32, int32_t N, int64_t d, const int32_t *psi,
   if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
   a.spb = ceil_div(a.nslices, nsr);
   a.nsr = ceil_div(ceil_div(a.nslices, a.spb), 8) * 8;
-  return f32 ? launch_mx<float>(a, KS, lds, stream) : launch_mx<uint16_t>(a, KS, lds, stream);
+  if (f32) return launch_mx<float, 64>(a, KS, lds, stream);
+  return win ? launch_mx<uint16_t, 128>(a, KS, lds, stream) : launch_mx<uint16_t, 64>(a, KS, lds, stream);
 }
 
 }  // namespace gcx

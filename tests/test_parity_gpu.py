@@ -389,7 +389,7 @@ def test_encode_matrix_rows_spilled_union():
 MX_WL = Workload(name="mx_m200_d4000_bf16", N=200, m=200, s=19, d=4000, P=40, ells=(1, 2, 4),
                  g_dtype="bf16", pattern="uniform", forced_zero=30)
 MX_CASES = [
-    (MX_WL, 1, 1), (MX_WL, 1, 3), (MX_WL, 1, 8), (MX_WL, 2, 16), (MX_WL, 4, 33),
+    (MX_WL, 1, 1), (MX_WL, 1, 3), (MX_WL, 1, 8), (MX_WL, 2, 16), (MX_WL, 4, 33), (MX_WL, 4, 130),
     (dataclasses.replace(MX_WL, name="mx_m70_d4001_bf16", N=70, m=70, s=9, d=4001), 3, 8),   # ragged, 70 % 4
     (dataclasses.replace(MX_WL, name="mx_m100_d81920_bf16", N=100, m=100, s=9, d=2048 * 40), 2, 5),
     (dataclasses.replace(MX_WL, name="mx_m200_d1024_bf16", d=1024), 8, 4),    # too many rows: other path
@@ -399,9 +399,10 @@ MX_CASES = [
 @pytest.mark.parametrize("wl,ell,count", MX_CASES, ids=[f"{w.name}-l{e}-P{c}" for w, e, c in MX_CASES])
 def test_encode_bf16_matrix_cores(wl, ell, count):
     """bf16 gradients on the bf16 matrix cores: 1 to 33 patterns per call (32 / 8 / 4 / 2 / 1
-    workers per tile, two pattern tiles), ragged d and ell not dividing d (element-wise
-    staging), a group count that does not divide m, straggler rows untouched; and a shape
-    whose staged rows do not fit (ell = 8), which takes the worker-group path."""
+    workers per tile, two pattern tiles), 128-candidate windows (ell = 2 to 4; 130 patterns:
+    a full window of 128 patterns and one of 2), ragged d and ell not dividing d
+    (element-wise staging), a group count that does not divide m, straggler rows untouched;
+    and a shape whose staged rows do not fit (ell = 8), which takes the worker-group path."""
     O, order, _, _ = tables(wl)
     _encode_against_oracle(O, order, patterns(wl, count), gen.shared_R(wl.m, ell), given_G(wl), "bf16",
                            ell, wl.d)
@@ -409,8 +410,8 @@ def test_encode_bf16_matrix_cores(wl, ell, count):
 
 def test_encode_bf16_matrix_cores_misaligned_and_spilled_union():
     """G one element off 16-byte alignment (element-wise staging); and a random 16-regular
-    support ordered by Algorithm 2, whose 8-worker groups use more chunks than their slots,
-    so each block walks its workers one at a time."""
+    support ordered by Algorithm 2, whose worker groups use more chunks than their slots,
+    so each block walks its workers one at a time (64- and 128-candidate windows)."""
     import oracle.ordering as OO
     wl = dataclasses.replace(MX_WL, name="mx_shift_m200_d4096_bf16", d=4096)
     O, order, _, _ = tables(wl)
@@ -424,6 +425,8 @@ def test_encode_bf16_matrix_cores_misaligned_and_spilled_union():
     psi = g.integers(0, nu + 1, size=(4, m)).astype(np.int32)
     G = gen.f32_to_bf16_bits(g.standard_normal((m, d)).astype(np.float32))
     _encode_against_oracle(O2.astype(np.int64), order2, psi, gen.shared_R(m, 1), G, "bf16", 1, d)
+    # ell = 2: 128-candidate windows (4 patterns x 32 workers), whose unions spill too
+    _encode_against_oracle(O2.astype(np.int64), order2, psi, gen.shared_R(m, 2), G, "bf16", 2, d)
 
 
 @pytest.mark.parametrize("wl,ell", [(TINY, 2), (GROUP_CASES[3][0], 2)], ids=["all-chunk", "worker-group"])
