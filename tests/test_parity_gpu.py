@@ -119,6 +119,41 @@ def test_decode_parity_large_least_squares(ell):
     check_decode(LARGE, psi, gen.shared_R(LARGE.m, ell))
 
 
+@pytest.mark.parametrize("m", [200, 300])
+def test_decode_cyclic_streamed_patterns(m):
+    """The cyclic ell = 1 decode with more patterns than resident waves, so each wave walks
+    several patterns (m = 200 and m = 300 workers: up to and past four psi entries per lane),
+    and invalid patterns inside the walk: integers for every pattern, coefficients on sampled
+    ones (the first, both sides of the first waves' second pattern, the invalid ones'
+    neighbours, the last)."""
+    wl = Workload(name=f"cyc_m{m}", N=m, m=m, s=9, d=64, P=20000, ells=(1,), pattern="uniform")
+    O, order, holder, hpos = tables(wl)
+    psi = patterns(wl, wl.P).copy()
+    bad = [9000, 9001, 15555]
+    psi[9000, 3] = wl.delta + 1
+    psi[9001, m - 1] = -1
+    psi[15555, 0] = wl.delta + 7
+    R = gen.shared_R(m, 1)
+    cov, dec, cerr, Bc = run_decode(wl, psi, R)
+    ok = np.ones(wl.P, dtype=bool)
+    ok[bad] = False
+    assert (dec[bad] == gcx.GC_DEC_INVALID).all() and (Bc[bad] == 0).all()
+    ref = np.zeros((wl.P, wl.N), dtype=np.int64)
+    for t in range(wl.delta):
+        ref += psi[:, (np.arange(wl.N) - t) % m] > t  # worker (i - t) mod N holds chunk i at position t
+    assert (cov[ok] == ref[ok]).all()
+    assert (dec[ok] == (ref[ok] >= 1).all(axis=1)).all()
+    assert (cerr[ok] == np.maximum(0, 1 - ref[ok]).sum(axis=1)).all()
+    rng = np.random.default_rng(37)
+    sample = sorted(set([0, 1, 4095, 4096, 6143, 6144, 6145, 8191, 8192, 8999, 9002, 15554, 15556,
+                         wl.P - 2, wl.P - 1] + rng.choice(wl.P, 9, replace=False).tolist()) - set(bad))
+    Bc_ref, kappa = R_.coefficients(O, psi[sample], R)
+    bound = R_.bc_bound(Bc_ref, kappa, O)
+    diff = np.abs(Bc[sample].astype(np.float64) - Bc_ref)
+    worst = np.unravel_index(np.argmax(diff - bound), diff.shape)
+    assert (diff <= bound).all(), f"Bc off at pattern {sample[worst[0]]}, {worst[1:]}"
+
+
 def test_decode_edge_patterns():
     """No worker done, all done, single worker done, s = 0, P not a multiple of 4."""
     wl = dataclasses.replace(TINY, name="tiny_edges")
@@ -580,16 +615,19 @@ def test_chunk_grads_many_points_mfma(wl, b):
 
 
 def test_chunk_grads_mfma_ragged_tiles():
-    """Row, point and column counts that are not multiples of the 128 x 128 tiles."""
-    wl = Workload(name="ragged_mfma", N=3, m=3, s=1, d=1000, P=1, ells=(1,), n=37, loss="logistic",
-                  x_std=0.05, w_std=0.1)
-    X, y, _ = gen.regression_data(wl)
-    for b in (20, 132):
-        W = gen.eval_points(wl, b)
-        G = host(gcx.gc_chunk_grads(dev(X), dev(y), dev(W), gcx.GC_LOSS_LOGISTIC))
-        G_ref = R_.chunk_grads(X, y, W, "logistic")
-        rel = np.linalg.norm(G - G_ref, axis=-1) / np.linalg.norm(G_ref, axis=-1)
-        assert rel.max() <= 1e-5, (b, rel.max())
+    """Row, point and column counts that are not multiples of the 128 x 128 tiles; with 7
+    chunks of d = 9000, more output tiles than resident blocks, so each block of G = U^T X
+    walks several tiles (ragged ones among them) as one stream of stages."""
+    for N, d, bs in ((3, 1000, (20, 132)), (7, 9000, (132, 256))):
+        wl = Workload(name=f"ragged_mfma_N{N}_d{d}", N=N, m=N, s=1, d=d, P=1, ells=(1,), n=37,
+                      loss="logistic", x_std=0.05, w_std=0.1)
+        X, y, _ = gen.regression_data(wl)
+        for b in bs:
+            W = gen.eval_points(wl, b)
+            G = host(gcx.gc_chunk_grads(dev(X), dev(y), dev(W), gcx.GC_LOSS_LOGISTIC))
+            G_ref = R_.chunk_grads(X, y, W, "logistic")
+            rel = np.linalg.norm(G - G_ref, axis=-1) / np.linalg.norm(G_ref, axis=-1)
+            assert rel.max() <= 1e-5, (N, d, b, rel.max())
 
 
 # ---------------------------------------------------------------------------
