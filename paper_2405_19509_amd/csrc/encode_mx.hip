@@ -55,6 +55,10 @@ constexpr int kMxRowBytes = kMxW * 2 + 16;   // staged row stride: padded so row
 constexpr int kMxfMaxWideKS = 3;             // fp32: 512-wide slices (1024 threads) up to 3 K steps
 static_assert(kMxW == (kMxThreads / 64) * 64 && kMxW * 2 == 64 * 16, "bf16: two 32-wide tiles per wave, 16 bytes per lane and staged row");
 constexpr int kMxMaxKS = 6;                  // K steps of 16 (at most 96 staged rows)
+// slices a block walks at most: runs of 32 wrote T 3-8% faster than the 128-373-slice runs
+// that about 16 blocks per CU gave at d = 2^20 and 2^24 (a store-only kernel with this
+// grid showed the same: its write rate rose with the number of shorter blocks)
+constexpr int64_t kMxSliceRun = 32;
 // bf16: 128-candidate windows (256-wide slices, one tile per wave) where a 64-candidate
 // window would need this many K steps
 constexpr int kMxWinKS = 3;
@@ -630,12 +634,14 @@ int encode_mx(const void *G, bool f32, int32_t N, int64_t d, const int32_t *psi,
   const int KS = q.KS, W = q.W;
   const size_t lds = q.lds;
   a.nslices = int(ceil_div(a.L, W));
-  // slice ranges: a multiple of 8 (one share per XCD), about 16 blocks per CU in all
+  // slice ranges: a multiple of 8 (one share per XCD), at least about 16 blocks per CU in
+  // all, and at most kMxSliceRun slices each
   const int64_t units = int64_t(a.ngroups) * a.ntp;
   const int64_t want = 16 * int64_t(cu_count());
   int64_t nsr = ceil_div(ceil_div(want, units), 8) * 8;
   if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
   a.spb = ceil_div(a.nslices, nsr);
+  if (a.spb > kMxSliceRun) a.spb = kMxSliceRun;
   a.nsr = ceil_div(ceil_div(a.nslices, a.spb), 8) * 8;
   if (f32) return launch_mx<float, 64>(a, KS, lds, stream);
   return win ? launch_mx<uint16_t, 128>(a, KS, lds, stream) : launch_mx<uint16_t, 64>(a, KS, lds, stream);
