@@ -213,7 +213,7 @@ ENC_CASES = [
     (TINY, 1, 100), (TINY, 2, 100), (TINY, 3, 100),
     (SMALL, 1, 40), (SMALL, 2, 40),
     (HEADLINE, 1, 12), (HEADLINE, 2, 12),
-    (BANDWIDTH_D16, 1, 6), (BANDWIDTH_D16, 8, 6),
+    (BANDWIDTH_D16, 1, 6), (BANDWIDTH_D16, 2, 6), (BANDWIDTH_D16, 8, 6),
     (LARGE_D16, 1, 3), (LARGE_D16, 2, 3),
     (RAGGED, 1, 37), (RAGGED, 3, 37), (RAGGED_BF16, 3, 37),
 ]
