@@ -194,7 +194,7 @@ int gc_decode_coeffs(const int32_t *psi, int64_t P, int32_t N, int32_t m, const 
  * gc_decode_coeffs); T [P][m][L] fp32 device.  fp32 accumulation.  psi is
  * clamped to [0, delta] and padded order slots are skipped.  G must be finite:
  * where the sums run on the matrix cores (bf16 G past the smallest shapes, fp32 G
- * from delta*ell >= 16 terms), a coefficient past a pattern's prefix or of a chunk
+ * from delta*ell >= 32 terms), a coefficient past a pattern's prefix or of a chunk
  * the worker does not hold enters as zero (and zero times a non-finite value is
  * not zero).  Accuracy per output, M = sum over its terms of |Bc||g| and
  * u = 2^-24: within u M plus the fp32 accumulation of 3 psi*ell products (bf16

@@ -248,9 +248,9 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs a) {
 // patterns, the tile rows are 16 (pattern, worker) pairs and its K the group's staged
 // chunk blocks (v_mfma_f32_16x16x4f32).
 // fp32 chunk gradients take the bf16 matrix-core encode from this many terms per output
-// (measured at m = 100, d = 2^20: at delta*ell = 10 the vector path writes 7% faster, at 20
-// the matrix cores 5% faster, at 80 by far)
-constexpr int kMxF32Terms = 16;
+// (measured at m = 100, d = 2^20: at delta*ell = 10 the vector path writes 7% faster; at 20
+// the two are within a few percent either way, at 80 the matrix cores win by far)
+constexpr int kMxF32Terms = 32;
 constexpr int kGrpThreads = 512;
 constexpr int kGrpWaves = kGrpThreads / kWave;
 constexpr size_t kGrpLds = 72 * 1024;     // per block: two blocks per CU
