@@ -51,7 +51,6 @@ namespace {
 
 constexpr int kMxThreads = 512;              // bf16, and fp32 with more than 3 K steps
 constexpr int kMxW = 512;                    // positions per slice (1 KB of bf16 per staged row)
-constexpr int kMxRowBytes = kMxW * 2 + 16;   // staged row stride: padded so rows 8 apart differ in bank
 constexpr int kMxfMaxWideKS = 3;             // fp32: 512-wide slices (1024 threads) up to 3 K steps
 static_assert(kMxW == (kMxThreads / 64) * 64 && kMxW * 2 == 64 * 16, "bf16: two 32-wide tiles per wave, 16 bytes per lane and staged row");
 constexpr int kMxMaxKS = 6;                  // K steps of 16 (at most 96 staged rows)
@@ -113,7 +112,7 @@ struct MxArgs {
   float *T;
   bool stage16;   // bf16: G 16-byte aligned and d, L multiples of 8; fp32: 8-byte, multiples of 2
   int J;          // workers per window
-  int PB;         // patterns per window (J * PB = 64 candidate rows)
+  int PB;         // patterns per window (J * PB = 64 or 128 candidate rows, at most)
   int ngroups;
   int64_t ntp;    // pattern windows
   int slots;      // union slots staged per block
@@ -135,10 +134,11 @@ struct MxLayout {
   static constexpr int NT = CW / 32;      // row tiles at most
   // fp32: one 32-wide tile per wave, 2 KB row segments of T per slice (16 waves) while the
   // staged rows fit, else 256 positions (8 waves); bf16: two tiles per wave, 512 positions
+  // (128-candidate windows: one tile per wave, 256 positions)
   static constexpr int THREADS = F32 && KS <= kMxfMaxWideKS ? 1024 : kMxThreads;
   static constexpr int WAVES = THREADS / 64;
   static constexpr int W = F32 || WIN ? 32 * WAVES : kMxW;  // positions per slice
-  static constexpr int RB = W * 2 + 16;              // bf16: staged row stride in bytes
+  static constexpr int RB = W * 2 + 16;  // bf16: staged row stride in bytes, padded so rows 8 apart differ in bank
   static constexpr int BS = Kp + 4;                  // fp32: floats per staged position
   static constexpr size_t slice_bytes = F32 ? size_t(W) * BS * 4 : size_t(Kp) * RB;
   // bf16 from 4 K steps on the staged rows allow one block per CU: registers for the K loop
