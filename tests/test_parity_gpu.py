@@ -334,6 +334,8 @@ def test_encode_worker_groups(wl, ell, count):
 # matrix-core encode: at least one full 32-pattern tile and delta*ell >= 32 terms per output
 MF_CASES = [
     (Workload(name="mf_m100_d4096", N=100, m=100, s=9, d=4096, P=40, ells=(8,), pattern="uniform"), 8, 40),
+    # fp32 on the bf16 matrix cores: two full 64-pattern windows and one of 2, odd L
+    (Workload(name="mf_m100_d2052", N=100, m=100, s=9, d=2052, P=130, ells=(8,), pattern="uniform"), 8, 130),
     (Workload(name="mf_m200_d2001_bf16", N=200, m=200, s=7, d=2001, P=33, ells=(4,), g_dtype="bf16",
               pattern="uniform"), 4, 33),
 ]
