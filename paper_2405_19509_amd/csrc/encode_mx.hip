@@ -641,7 +641,9 @@ int encode_mx(const void *G, bool f32, int32_t N, int64_t d, const int32_t *psi,
   int64_t nsr = ceil_div(ceil_div(want, units), 8) * 8;
   if (nsr > ceil_div(a.nslices, 8) * 8) nsr = ceil_div(a.nslices, 8) * 8;
   a.spb = ceil_div(a.nslices, nsr);
-  if (a.spb > kMxSliceRun) a.spb = kMxSliceRun;
+  // shorter runs while the grid stays within the launch limits (1024 threads per block at most)
+  if (a.spb > kMxSliceRun && ceil_div(ceil_div(a.nslices, kMxSliceRun), 8) * 8 * units <= 0xffffffffLL / 1024)
+    a.spb = kMxSliceRun;
   a.nsr = ceil_div(ceil_div(a.nslices, a.spb), 8) * 8;
   if (f32) return launch_mx<float, 64>(a, KS, lds, stream);
   return win ? launch_mx<uint16_t, 128>(a, KS, lds, stream) : launch_mx<uint16_t, 64>(a, KS, lds, stream);
