@@ -18,7 +18,7 @@
 //
 // Layout: a block owns a group of J consecutive workers, a window of PB patterns
 // (J * PB = 64 or 128 candidate rows (pattern, worker), candidate r = pb * J + jb) and a
-// range of slices of x walked in turn.  The window's transmitting rows (psi > 0) are
+// range of at most 32 slices of x walked in turn.  The window's transmitting rows (psi > 0) are
 // compacted into full 32-row tiles (stragglers cost nothing), whose coefficients, split
 // into three bf16 planes, are built once per block.  Per slice the block stages the slices
 // of the group's union of chunks (J + delta - 1 chunks under the cyclic order), one row per
@@ -31,10 +31,10 @@
 //         row written nearly halve; each wave takes one 32-wide column, gathered once per K
 //         step for all (up to four) row tiles.  From 4 K steps on a block fills a CU's LDS
 //         and the K loop is unrolled into the registers that frees;
-//   fp32: 256-wide slices staged through registers with the staged rows fastest, so that a
-//         lane's eight K values of one position are two 16-byte reads, split once per slice
-//         for both row tiles; each wave takes one 32-position tile, six MFMAs per row tile
-//         and K step.
+//   fp32: 512-wide slices (256-wide from 4 K steps on) staged through registers with the
+//         staged rows fastest, so that a lane's eight K values of one position are two
+//         16-byte reads, split once per slice for both row tiles; each wave takes one
+//         32-position tile, six MFMAs per row tile and K step.
 // Stores are 4 bytes per lane, two 128-byte row segments per instruction, non-temporal;
 // rows of workers that transmit nothing (psi = 0) are not written.  Blocks of a slice range
 // run back to back on one XCD (round-robin dispatch), so its L2 serves the groups'
@@ -54,9 +54,9 @@ constexpr int kMxW = 512;                    // positions per slice (1 KB of bf1
 constexpr int kMxfMaxWideKS = 3;             // fp32: 512-wide slices (1024 threads) up to 3 K steps
 static_assert(kMxW == (kMxThreads / 64) * 64 && kMxW * 2 == 64 * 16, "bf16: two 32-wide tiles per wave, 16 bytes per lane and staged row");
 constexpr int kMxMaxKS = 6;                  // K steps of 16 (at most 96 staged rows)
-// slices a block walks at most: runs of 32 wrote T 3-8% faster than the 128-373-slice runs
-// that about 16 blocks per CU gave at d = 2^20 and 2^24 (a store-only kernel with this
-// grid showed the same: its write rate rose with the number of shorter blocks)
+// slices a block walks at most: runs of 32 wrote T up to 8% faster than the 128-373-slice
+// runs that about 16 blocks per CU gave at d = 2^20 and 2^24 (a store-only kernel with
+// this grid showed the same: its write rate rose with the number of shorter blocks)
 constexpr int64_t kMxSliceRun = 32;
 // bf16: 128-candidate windows (256-wide slices, one tile per wave) where a 64-candidate
 // window would need this many K steps
