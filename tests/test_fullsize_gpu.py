@@ -217,3 +217,64 @@ def test_large_full_size(variant, ells):
     check_sampled(O, order, psi[p0:p0 + 1], R, G, "bf16", T, ghat, [0],
                   np.random.default_rng(20 + ell).choice(L, 48, replace=False), ell)
     assert np.isfinite(host(sqerr)).all()
+
+
+_LARGE_G = {}
+
+
+def _large_G():
+    if "G" not in _LARGE_G:
+        _LARGE_G["G"] = gen.given_G(LARGE, threads=THREADS)
+    return _LARGE_G["G"]
+
+
+@pytest.mark.parametrize("variant,ell,per_call", [("exact", 1, 16), ("exact", 2, 32), ("ls", 1, 16),
+                                                  ("ls", 2, 32), ("ls", 4, 64)])
+def test_large_encode_bench_launch(variant, ell, per_call):
+    """m = 200, d = 2^24, bf16 chunk gradients: the first call of each of the bench's configs
+    rows (16 / 32 / 64 patterns per call: 64- and 128-candidate windows, runs of 32 slices,
+    T up to 215 GB), T and the estimate on sampled patterns and positions (slice and run
+    boundaries among them)."""
+    wl = LARGE
+    O, order, holder, hpos = tables(wl)
+    psi = gen.psi(wl, count=per_call, variant=variant)
+    R = gen.shared_R(wl.m, ell)
+    G = _large_G()
+    Gd = dev(G.view(np.int16)).view(torch.bfloat16)
+    pd = dev(psi)
+    _, _, _, Bc = gcx.gc_decode_coeffs(pd, dev(order), dev(holder), dev(hpos), dev(R))
+    T = gcx.gc_encode(Gd, pd, dev(order), Bc)
+    ghat, sqerr = gcx.gc_reconstruct(T, dev(R), wl.d, psi=pd, gsum=gcx.gc_sum_chunks(Gd))
+    L = -(-wl.d // ell)
+    rng = np.random.default_rng(50 + ell)
+    xs = sorted(set([0, 255, 256, 511, 512, 8191, 8192, L - 257, L - 1] + rng.choice(L, 40, replace=False).tolist()))
+    pats = sorted(set([0, per_call // 2, per_call - 1]))
+    check_sampled(O, order, psi, R, G, "bf16", T, ghat, pats, xs, ell)
+    assert np.isfinite(host(sqerr)).all()
+    del T, ghat, Bc, Gd
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("ell,per_call", [(1, 256), (2, 512), (8, 1024)])
+def test_bandwidth_encode_bench_launch(ell, per_call):
+    """m = 100, d = 2^20, fp32 chunk gradients: the first call of each of the bench's configs
+    rows (256 / 512 / 1,024 patterns per call: the worker-group layout at ell = 1, 2 and the
+    matrix-core encode at ell = 8), T and the estimate on sampled patterns and positions."""
+    wl = BANDWIDTH
+    O, order, holder, hpos = tables(wl)
+    psi = gen.psi(wl, count=per_call)
+    R = gen.shared_R(wl.m, ell)
+    G = gen.given_G(wl, threads=THREADS)
+    Gd = dev(G)
+    pd = dev(psi)
+    _, _, _, Bc = gcx.gc_decode_coeffs(pd, dev(order), dev(holder), dev(hpos), dev(R))
+    T = gcx.gc_encode(Gd, pd, dev(order), Bc)
+    ghat, sqerr = gcx.gc_reconstruct(T, dev(R), wl.d, psi=pd, gsum=gcx.gc_sum_chunks(Gd))
+    L = -(-wl.d // ell)
+    rng = np.random.default_rng(60 + ell)
+    xs = sorted(set([0, 255, 256, 511, 512, 1023, 1024, L - 257, L - 1] + rng.choice(L, 40, replace=False).tolist()))
+    pats = sorted(set([0, 1, per_call // 2, per_call - 1]))
+    check_sampled(O, order, psi, R, G, "f32", T, ghat, pats, xs, ell)
+    assert np.isfinite(host(sqerr)).all()
+    del T, ghat, Bc, Gd
+    torch.cuda.empty_cache()
